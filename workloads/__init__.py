@@ -1,0 +1,371 @@
+"""Seeded synthetic inputs for batched paged-KV attention with per-request masks.
+
+This module is shared by the tests, the benchmark and the smoke check.  It
+holds no attention arithmetic: it only draws request lengths, lays requests
+out in a paged KV pool, writes mask descriptors and draws Q/K/V values.  Both
+the CPU oracle and the HIP path consume what it returns; neither is imported
+here.
+
+Workload shapes stand in for the serving scenarios the paper runs (it gives no
+per-layer attention shapes and its datasets are not used):
+
+* ``tiny_causal_f32``   - a tiny causal prefill in fp32 (parity case).
+* ``decode_bf16``       - one new token per request over a long context, GQA 7:1
+                          (autoregressive decode inside a ``DynamicLoop``,
+                          Sec. 3.1 "Loop optimizations"; Sec. 4.2 / 4.3).
+* ``text_latent_bf16``  - causal text prefix followed by a full-attention latent
+                          block (BAGEL's flow loop over latents, Sec. 3.1
+                          listing of the image-generation Walk; Sec. 4.1).
+* ``stream_window_bf16``- 16-token streamed chunks over a long context under a
+                          sliding window (streaming edges, Sec. 3.1 "Flexible
+                          chunk policies").
+* ``rollout_bf16``      - K candidate rollouts appending frame blocks over one
+                          shared context whose pages every block table points
+                          to (V-JEPA 2 rollout and MPC, Sec. 4.4 and App. A).
+* ``mixed``             - requests of all the kinds above in one launch (one
+                          ``LLM`` replica serving every Walk, Sec. 3.2).
+
+Descriptor layout (mirrors the C structs of the library boundary):
+
+* ``seqs``      int32 ``[n, 3]``: ``q_len, kv_len, q_start``.  Queries sit at the
+                last ``q_len`` positions of the request's ``kv_len`` keys.
+* ``masks``     int32 ``[n, 3]``: ``seg_begin, seg_count, window``.
+* ``segments``  int32 ``[S, 4]``: ``start, len, kind, block``; kinds are
+                ``CAUSAL`` (0), ``FULL`` (1) and ``BLOCKS`` (2).
+* ``block_table`` int32 ``[n, max_blocks]``: physical page of each logical page.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import numpy as np
+
+SEG_CAUSAL = 0
+SEG_FULL = 1
+SEG_BLOCKS = 2
+PAGE = 16
+
+# Sub-seed offsets: every random field has its own stream.
+_SUB_LENGTHS = 1
+_SUB_PERM = 2
+_SUB_Q = 3
+_SUB_K = 4
+_SUB_V = 5
+
+
+@dataclasses.dataclass
+class Batch:
+    """Descriptors of one attention launch (no tensor data)."""
+
+    name: str
+    num_qo_heads: int
+    num_kv_heads: int
+    head_dim: int
+    dtype: str  # "f32" or "bf16"
+    seqs: np.ndarray
+    masks: np.ndarray
+    segments: np.ndarray
+    block_table: np.ndarray
+    num_pages: int
+    page_size: int = PAGE
+    sm_scale: float = 0.0
+    seed: int = 0
+
+    def __post_init__(self):
+        if self.sm_scale == 0.0:
+            self.sm_scale = float(1.0 / np.sqrt(self.head_dim))
+
+    @property
+    def num_seqs(self) -> int:
+        return int(self.seqs.shape[0])
+
+    @property
+    def total_q(self) -> int:
+        if self.num_seqs == 0:
+            return 0
+        return int((self.seqs[:, 0] + self.seqs[:, 2]).max())
+
+    def seq_segments(self, r: int) -> np.ndarray:
+        b, c, _ = self.masks[r]
+        return self.segments[b:b + c]
+
+
+def _rng(seed: int, sub: int) -> np.random.Generator:
+    return np.random.default_rng([int(seed), int(sub)])
+
+
+def _layout_pages(kv_lens, pool_pages: Optional[int], rng, shared_prefix_pages: int = 0):
+    """Assign physical pages to requests from a seeded permutation of the pool.
+
+    Pages are handed out in permutation order; the first ``shared_prefix_pages``
+    of the permutation are referenced by every request's first logical pages.
+    """
+    need = [(int(L) + PAGE - 1) // PAGE for L in kv_lens]
+    own = [n - shared_prefix_pages for n in need]
+    total = shared_prefix_pages + sum(own)
+    pool = total if pool_pages is None else int(pool_pages)
+    if pool < total:
+        raise ValueError("page pool too small")
+    perm = rng.permutation(pool).astype(np.int32)
+    max_blocks = max(need) if need else 1
+    bt = np.full((len(kv_lens), max(max_blocks, 1)), -1, dtype=np.int32)
+    shared = perm[:shared_prefix_pages]
+    cur = shared_prefix_pages
+    for r, n in enumerate(own):
+        bt[r, :shared_prefix_pages] = shared
+        bt[r, shared_prefix_pages:shared_prefix_pages + n] = perm[cur:cur + n]
+        cur += n
+    return bt, pool
+
+
+def _finish(name, hq, hkv, d, dtype, q_lens, kv_lens, seg_lists, windows, bt, pool, seed):
+    n = len(q_lens)
+    seqs = np.zeros((n, 3), dtype=np.int32)
+    masks = np.zeros((n, 3), dtype=np.int32)
+    segs = []
+    qs = 0
+    for r in range(n):
+        seqs[r] = (q_lens[r], kv_lens[r], qs)
+        qs += q_lens[r]
+        masks[r] = (len(segs), len(seg_lists[r]), windows[r])
+        segs.extend(seg_lists[r])
+    segments = np.array(segs, dtype=np.int32).reshape(-1, 4)
+    return Batch(name=name, num_qo_heads=hq, num_kv_heads=hkv, head_dim=d, dtype=dtype,
+                 seqs=seqs, masks=masks, segments=segments, block_table=bt,
+                 num_pages=pool, seed=seed)
+
+
+# --------------------------------------------------------------------------
+# The five workloads at full size, plus scaled-down variants for tests.
+# --------------------------------------------------------------------------
+
+def tiny_causal_f32(seed: int = 0) -> Batch:
+    """4 causal prefills of lengths 17, 33, 64, 5; 2 query heads over 1 KV head;
+    head_dim 64; fp32; pages permuted by seed."""
+    lens = [17, 33, 64, 5]
+    bt, pool = _layout_pages(lens, None, _rng(seed, _SUB_PERM))
+    segs = [[(0, L, SEG_CAUSAL, 0)] for L in lens]
+    return _finish("tiny_causal_f32", 2, 1, 64, "f32", lens, lens, segs, [0] * 4, bt, pool, seed)
+
+
+def decode_bf16(seed: int = 0, n: int = 64, lmin: int = 512, lmax: int = 8192,
+                hq: int = 28, hkv: int = 4, d: int = 128, pool_pages: Optional[int] = 40000) -> Batch:
+    """n requests, each one new query token over a context of length
+    L ~ U{lmin..lmax} (the new token's K/V is already cached: kv_len = L)."""
+    L = _rng(seed, _SUB_LENGTHS).integers(lmin, lmax + 1, size=n)
+    kv = [int(x) for x in L]
+    bt, pool = _layout_pages(kv, pool_pages, _rng(seed, _SUB_PERM))
+    segs = [[(0, x, SEG_CAUSAL, 0)] for x in kv]
+    return _finish("decode_bf16", hq, hkv, d, "bf16", [1] * n, kv, segs, [0] * n, bt, pool, seed)
+
+
+def text_latent_bf16(seed: int = 0, n: int = 8, text: int = 256, latent: int = 4096,
+                     hq: int = 28, hkv: int = 4, d: int = 128) -> Batch:
+    """n prefills of a causal text prefix followed by a latent block with full
+    attention inside the block and full view of the prefix."""
+    L = text + latent
+    kv = [L] * n
+    bt, pool = _layout_pages(kv, None, _rng(seed, _SUB_PERM))
+    segs = [[(0, text, SEG_CAUSAL, 0), (text, latent, SEG_FULL, 0)] for _ in range(n)]
+    return _finish("text_latent_bf16", hq, hkv, d, "bf16", kv, kv, segs, [0] * n, bt, pool, seed)
+
+
+def stream_window_bf16(seed: int = 0, n: int = 256, chunk: int = 16, cmin: int = 1024,
+                       cmax: int = 16384, window: int = 1024, hq: int = 16, hkv: int = 8,
+                       d: int = 128) -> Batch:
+    """n requests each appending a causal chunk over an existing context of
+    length C ~ U{cmin..cmax}, under a sliding window of ``window`` keys."""
+    C = _rng(seed, _SUB_LENGTHS).integers(cmin, cmax + 1, size=n)
+    kv = [int(c) + chunk for c in C]
+    bt, pool = _layout_pages(kv, None, _rng(seed, _SUB_PERM))
+    segs = [[(0, x, SEG_CAUSAL, 0)] for x in kv]
+    return _finish("stream_window_bf16", hq, hkv, d, "bf16", [chunk] * n, kv, segs,
+                   [window] * n, bt, pool, seed)
+
+
+def rollout_bf16(seed: int = 0, n: int = 300, prefix: int = 2048, frames: int = 4,
+                 frame: int = 256, hq: int = 16, hkv: int = 16, d: int = 64) -> Batch:
+    """n candidate rollouts sharing one context of ``prefix`` tokens (its pages
+    are referenced by every block table) and each appending ``frames`` frames of
+    ``frame`` tokens: full attention inside a frame, causal across frames, full
+    view of the prefix.  Only the appended frames are queried."""
+    if prefix % PAGE:
+        raise ValueError("shared prefix must be page aligned")
+    q = frames * frame
+    L = prefix + q
+    kv = [L] * n
+    bt, pool = _layout_pages(kv, None, _rng(seed, _SUB_PERM), shared_prefix_pages=prefix // PAGE)
+    segs = [[(0, prefix, SEG_FULL, 0), (prefix, q, SEG_BLOCKS, frame)] for _ in range(n)]
+    return _finish("rollout_bf16", hq, hkv, d, "bf16", [q] * n, kv, segs, [0] * n, bt, pool, seed)
+
+
+def mixed(seed: int = 0, hq: int = 8, hkv: int = 2, d: int = 128, dtype: str = "bf16",
+          scale: int = 1) -> Batch:
+    """Requests of every kind in one launch: decode, text+latent prefill,
+    windowed chunks, frame-block rollouts over shared prefix pages, and a
+    block-causal request with a ragged final block."""
+    rng = _rng(seed, _SUB_LENGTHS)
+    q_lens, kv_lens, seg_lists, windows = [], [], [], []
+    # decode requests
+    for L in rng.integers(40, 700 * scale, size=3):
+        L = int(L)
+        q_lens.append(1); kv_lens.append(L); seg_lists.append([(0, L, SEG_CAUSAL, 0)]); windows.append(0)
+    # text + latent prefill
+    t, lat = 37, 160 * scale + 3
+    q_lens.append(t + lat); kv_lens.append(t + lat)
+    seg_lists.append([(0, t, SEG_CAUSAL, 0), (t, lat, SEG_FULL, 0)]); windows.append(0)
+    # windowed chunks
+    for C in rng.integers(100, 600 * scale, size=2):
+        C = int(C)
+        q_lens.append(16); kv_lens.append(C + 16); seg_lists.append([(0, C + 16, SEG_CAUSAL, 0)])
+        windows.append(96)
+    # block-causal with a ragged last block, queried partly
+    L = 211 * scale
+    q_lens.append(150 * scale); kv_lens.append(L)
+    seg_lists.append([(0, 19, SEG_CAUSAL, 0), (19, L - 19, SEG_BLOCKS, 48)]); windows.append(0)
+    kv_rollout_start = len(kv_lens)
+    # rollouts over one shared prefix (added last so the prefix pages are shared)
+    prefix, fr, nf = 64, 32, 3
+    n_roll = 3
+    for _ in range(n_roll):
+        q_lens.append(nf * fr); kv_lens.append(prefix + nf * fr)
+        seg_lists.append([(0, prefix, SEG_FULL, 0), (prefix, nf * fr, SEG_BLOCKS, fr)]); windows.append(0)
+    # page layout: non-rollout requests get private pages, rollouts share a prefix
+    prng = _rng(seed, _SUB_PERM)
+    need = [(x + PAGE - 1) // PAGE for x in kv_lens]
+    shared_pages = prefix // PAGE
+    own = [need[r] - (shared_pages if r >= kv_rollout_start else 0) for r in range(len(need))]
+    pool = sum(own) + shared_pages + 7  # a few unreferenced pages
+    perm = prng.permutation(pool).astype(np.int32)
+    bt = np.full((len(kv_lens), max(need)), -1, dtype=np.int32)
+    shared = perm[:shared_pages]
+    cur = shared_pages
+    for r in range(len(kv_lens)):
+        off = 0
+        if r >= kv_rollout_start:
+            bt[r, :shared_pages] = shared
+            off = shared_pages
+        bt[r, off:off + own[r]] = perm[cur:cur + own[r]]
+        cur += own[r]
+    return _finish("mixed", hq, hkv, d, dtype, q_lens, kv_lens, seg_lists, windows, bt, pool, seed)
+
+
+FULL_SIZE = {
+    "tiny_causal_f32": tiny_causal_f32,
+    "decode_bf16": decode_bf16,
+    "text_latent_bf16": text_latent_bf16,
+    "stream_window_bf16": stream_window_bf16,
+    "rollout_bf16": rollout_bf16,
+}
+
+
+def reduced(name: str, seed: int = 0) -> Batch:
+    """Scaled-down variant of a workload: same mask structure and head layout,
+    sizes small enough for the CPU oracle to finish in seconds while still
+    spanning several tiles and ragged tails."""
+    if name == "tiny_causal_f32":
+        return tiny_causal_f32(seed)
+    if name == "decode_bf16":
+        return decode_bf16(seed, n=9, lmin=1, lmax=1500, pool_pages=None)
+    if name == "text_latent_bf16":
+        return text_latent_bf16(seed, n=2, text=37, latent=300)
+    if name == "stream_window_bf16":
+        return stream_window_bf16(seed, n=7, cmin=1, cmax=700, window=100)
+    if name == "rollout_bf16":
+        return rollout_bf16(seed, n=5, prefix=64, frames=4, frame=40)
+    if name == "mixed":
+        return mixed(seed)
+    raise KeyError(name)
+
+
+# --------------------------------------------------------------------------
+# Tensor values.
+# --------------------------------------------------------------------------
+
+def tensor_shapes(b: Batch):
+    return {
+        "q": (b.total_q, b.num_qo_heads, b.head_dim),
+        "k_pages": (b.num_pages, b.page_size, b.num_kv_heads, b.head_dim),
+        "v_pages": (b.num_pages, b.page_size, b.num_kv_heads, b.head_dim),
+    }
+
+
+def make_tensors_numpy(b: Batch, seed: Optional[int] = None):
+    """Q/K/V iid N(0,1) drawn in float32 on the host (small batches only).
+    For bf16 batches the values are rounded to bf16 (nearest even) and returned
+    as float32 arrays holding exactly the bf16 values."""
+    seed = b.seed if seed is None else seed
+    out = {}
+    for name, sub in (("q", _SUB_Q), ("k_pages", _SUB_K), ("v_pages", _SUB_V)):
+        x = _rng(seed, sub).standard_normal(tensor_shapes(b)[name], dtype=np.float32)
+        if b.dtype == "bf16":
+            x = round_to_bf16(x)
+        out[name] = x
+    return out
+
+
+def round_to_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bf16 (ties to even); float32 result."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    lsb = (u >> 16) & 1
+    r = ((u + 0x7FFF + lsb) >> 16) << 16
+    return r.astype(np.uint32).view(np.float32).reshape(x.shape)
+
+
+def make_tensors_torch(b: Batch, device, seed: Optional[int] = None, poison_unused: bool = False):
+    """Q/K/V iid N(0,1) drawn with torch's generator on ``device`` (float32, then
+    rounded to the batch dtype).  With ``poison_unused`` every page slot that no
+    request references (unreferenced pages and the tail slots of each request's
+    last page) is set to NaN."""
+    import torch
+
+    seed = b.seed if seed is None else seed
+    dt = torch.float32 if b.dtype == "f32" else torch.bfloat16
+    g = torch.Generator(device=device)
+    out = {}
+    for name, sub in (("q", _SUB_Q), ("k_pages", _SUB_K), ("v_pages", _SUB_V)):
+        g.manual_seed(int(seed) * 1000003 + sub)
+        x = torch.randn(tensor_shapes(b)[name], generator=g, device=device, dtype=torch.float32)
+        out[name] = x.to(dt)
+        del x
+    if poison_unused:
+        used = used_slots(b)
+        mask = torch.from_numpy(~used).to(device)
+        for name in ("k_pages", "v_pages"):
+            out[name][mask] = float("nan")
+    return out
+
+
+def used_slots(b: Batch) -> np.ndarray:
+    """bool ``[num_pages, page_size]``: slots that hold a key of some request."""
+    used = np.zeros((b.num_pages, b.page_size), dtype=bool)
+    for r in range(b.num_seqs):
+        L = int(b.seqs[r, 1])
+        for t0 in range(0, L, b.page_size):
+            p = int(b.block_table[r, t0 // b.page_size])
+            used[p, :min(b.page_size, L - t0)] = True
+    return used
+
+
+def permute_pages(b: Batch, tensors: dict, seed: int):
+    """The same logical batch stored under a different physical page order:
+    page ``p`` moves to ``perm[p]`` and block tables are rewritten to match."""
+    perm = np.random.default_rng([seed, 99]).permutation(b.num_pages).astype(np.int32)
+    bt = b.block_table.copy()
+    valid = bt >= 0
+    bt[valid] = perm[bt[valid]]
+    nb = dataclasses.replace(b, block_table=bt)
+    inv = np.empty_like(perm)
+    inv[perm] = np.arange(b.num_pages, dtype=np.int32)
+    nt = dict(tensors)
+    for name in ("k_pages", "v_pages"):
+        x = tensors[name]
+        nt[name] = x[inv] if isinstance(x, np.ndarray) else x[_as_index(x, inv)]
+    return nb, nt
+
+
+def _as_index(x, idx):
+    import torch
+
+    return torch.from_numpy(idx.astype(np.int64)).to(x.device)
