@@ -1,0 +1,204 @@
+/*
+ * mstar_attn.h - batched variable-length attention over a paged KV cache,
+ * with a per-request segment mask, for AMD Instinct MI355X (gfx950).
+ *
+ * What is computed.  A launch serves many requests at once, each at its own
+ * point of its own traversal of the model graph (the paper's requests are
+ * series of Walks over one graph, Sec. 3.1, and one LLM replica is multiplexed
+ * across requests of every Walk, Sec. 3.2).  For every request r, query head
+ * h and query row i (position p = kv_len - q_len + i):
+ *
+ *   out[q_start+i][h][:] = sum_t softmax_t(s) * V_r[t][h / (Hq/Hkv)][:]
+ *   lse[q_start+i][h]    = ln sum_t exp(s_t),    s_t = sm_scale * <q, K_r[t]>
+ *
+ * over the keys t the row may see.  K_r[t] / V_r[t] are read in place from a
+ * shared page pool through the request's block table (paged attention inside
+ * the KVCacheEngine, Sec. 3.3; several contexts as labels over one page pool
+ * whose tables are read in place, Sec. 4.1; K rollout candidates over one
+ * shared context, Sec. 4.4 and App. A).  The paper does not define the masks;
+ * the segment model below is this library's stated reading.
+ *
+ * Mask model.  A request's keys [0, kv_len) are tiled, in order, by segments.
+ * Walking them assigns each position a block id: CAUSAL makes every token its
+ * own block, FULL makes the whole segment one block, BLOCKS(b) makes runs of
+ * b tokens one block each (the last run may be short).  Key t is visible to
+ * the row at position p iff block(t) <= block(p) and, when window W > 0,
+ * p - t < W (exactly W keys ending at p, plus later keys of p's own block).
+ * A row with no visible key gets out = 0 and lse = -inf.
+ *
+ * Memory layouts (all row-major, element type = params.dtype unless noted):
+ *   q, out        [total_q][Hq][head_dim]
+ *   lse           [total_q][Hq]  float32, natural log
+ *   k_pages/v_pages [num_pages][page_size][Hkv][head_dim]   ("NHD")
+ *   block_table   int32 [num_seqs][max_blocks_per_seq]
+ *
+ * Error convention.  Every int-returning call returns MSTAR_OK (0) or a
+ * negative MSTAR_ERR_* code and never throws or aborts; mstar_last_error()
+ * then gives a message for the calling thread.
+ */
+#ifndef MSTAR_ATTN_H
+#define MSTAR_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- codes -------------------------------------------------------------- */
+#define MSTAR_OK 0
+#define MSTAR_ERR_INVALID_ARG (-1) /* a descriptor or pointer violates this contract */
+#define MSTAR_ERR_UNSUPPORTED (-2) /* head_dim, page_size or dtype not built        */
+#define MSTAR_ERR_WORKSPACE (-3)   /* workspace missing or smaller than required    */
+#define MSTAR_ERR_HIP (-4)         /* a HIP runtime call failed (message has it)    */
+#define MSTAR_ERR_NOMEM (-5)       /* host or device allocation failed              */
+
+#define MSTAR_SEG_CAUSAL 0 /* every token its own block                        */
+#define MSTAR_SEG_FULL 1   /* the whole segment one block                      */
+#define MSTAR_SEG_BLOCKS 2 /* consecutive blocks of `block` tokens             */
+
+#define MSTAR_DTYPE_F32 0
+#define MSTAR_DTYPE_BF16 1
+
+#define MSTAR_FLAG_FORCE_SPLIT 1u /* split every key range into small chunks (exercises the merge) */
+#define MSTAR_FLAG_NO_SPLIT 2u    /* never split key ranges                                      */
+#define MSTAR_FLAG_HOST_ONLY 4u   /* plan on the host only: no device allocation or upload; for
+                                     inspection (stats, items, key ranges) without a GPU; fwd
+                                     rejects such a plan                                         */
+
+/* Bits of the sticky device error word (see mstar_attn_check). */
+#define MSTAR_DEVERR_PAGE_RANGE 1 /* a block-table entry was outside [0, num_pages) */
+
+/* ---- descriptors ---------------------------------------------------------- */
+
+/* One segment of a request's key range: positions [start, start+len). */
+typedef struct {
+    int32_t start;
+    int32_t len;
+    int32_t kind;  /* MSTAR_SEG_* */
+    int32_t block; /* block length for MSTAR_SEG_BLOCKS (> 0); ignored otherwise */
+} mstar_segment;
+
+/* A request's mask: segments [seg_begin, seg_begin+seg_count) of the segment
+ * array, which must tile [0, kv_len) in order; window = 0 means no window. */
+typedef struct {
+    int32_t seg_begin;
+    int32_t seg_count;
+    int32_t window;
+} mstar_mask_spec;
+
+/* A request: its queries are the last q_len of its kv_len positions (new
+ * tokens are already in the paged cache); they occupy packed rows
+ * [q_start, q_start+q_len) of q/out/lse.  Row ranges of different requests
+ * must not overlap.  Several requests may reference the same physical pages. */
+typedef struct {
+    int32_t q_len;
+    int32_t kv_len;
+    int32_t q_start;
+} mstar_seq_desc;
+
+typedef struct {
+    int32_t num_qo_heads;       /* Hq, a multiple of Hkv                          */
+    int32_t num_kv_heads;       /* Hkv                                            */
+    int32_t head_dim;           /* 64 or 128                                      */
+    int32_t page_size;          /* 16                                             */
+    int32_t dtype;              /* MSTAR_DTYPE_F32 or MSTAR_DTYPE_BF16            */
+    int32_t max_blocks_per_seq; /* row stride of block_table; kv_len <= 16 * this */
+    int32_t num_pages;          /* pages in the pool (bounds-checked on device)   */
+    uint32_t flags;             /* MSTAR_FLAG_*                                   */
+    float sm_scale;             /* score scale, typically 1/sqrt(head_dim)        */
+} mstar_attn_params;
+
+typedef struct mstar_plan mstar_plan_t;
+
+typedef struct {
+    int64_t visible_pairs;   /* (row, key) pairs the rows may see, summed over query heads */
+    int64_t prefill_items;   /* work items of the multi-row tile kernel                    */
+    int64_t decode_items;    /* work items of the few-row (decode / chunk) kernel           */
+    int64_t f32_items;       /* work items of the fp32 kernel                               */
+    int64_t merge_rows;      /* (row, head) outputs assembled from split partials           */
+    int64_t partial_slots;   /* fp32 partial rows in the workspace                          */
+    int64_t total_q;         /* packed query rows (max q_start + q_len)                     */
+    double plan_host_us;     /* host time spent building the plan                           */
+} mstar_plan_stats;
+
+/* ---- entry points -------------------------------------------------------- */
+
+/* Build the launch plan for one batch (host side; the attention plan the
+ * paper's workers build off the critical path, Sec. 3.3).  Reads descriptors
+ * only, never tensor data, and copies them, so the caller may free its arrays
+ * on return; thread-safe, so it can run on a side thread while the previous
+ * batch's fwd executes.  Derives each query row's visible key interval from
+ * its mask, cuts the batch into work items (multi-row tiles for long query
+ * spans, few-row items for decode-like requests, key ranges split into chunks
+ * when there are too few items to fill the GPU), orders them longest first,
+ * and uploads the work list with an async host-to-device copy enqueued on
+ * `upload_stream` (a hipStream_t; NULL = default stream).  The caller must
+ * order that upload before fwd (same stream, or synchronize).  Allocates
+ * device memory for the work list (owned by the plan).  On success *out is a
+ * new plan; on failure *out is NULL.
+ * Errors: INVALID_ARG (null pointer, Hq % Hkv != 0, q_len > kv_len, segments
+ * not tiling [0, kv_len), negative window, kv_len > 16 * max_blocks_per_seq,
+ * overlapping row ranges, ...), UNSUPPORTED (head_dim, page_size, dtype),
+ * NOMEM, HIP. */
+int mstar_attn_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
+                    const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segments,
+                    int32_t num_segs, void* upload_stream, mstar_plan_t** out);
+
+/* Bytes of device scratch fwd needs (fp32 partial outputs and their LSEs for
+ * split key ranges); 0 if nothing is split.  Returns 0 for a NULL plan. */
+size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan);
+
+/* Run the planned attention on `stream` (a hipStream_t; NULL = default).
+ * q, k_pages, v_pages, block_table: caller-owned device memory, read only;
+ * pages may be shared between requests.  out, lse: caller-owned device
+ * memory, written for every row of every request (rows of no request are
+ * untouched).  workspace: caller-owned device memory of at least
+ * mstar_attn_workspace_bytes(plan) bytes (may be NULL if that is 0); fwd
+ * overwrites it.  Enqueues at most four kernels; no allocation, no host
+ * synchronization and no host reads, so the call may be captured in a HIP
+ * graph.  The same plan may run with any tensors of the planned shapes.  Two
+ * fwd calls that overlap in time must use different workspaces.  Block-table
+ * entries outside [0, num_pages) are never dereferenced: they read as zeros
+ * and set MSTAR_DEVERR_PAGE_RANGE in the plan's device error word.
+ * Errors: INVALID_ARG (null tensor pointer, misaligned pointer), WORKSPACE,
+ * HIP (launch failure). */
+int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const void* k_pages,
+                   const void* v_pages, const int32_t* block_table, void* out, float* lse,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* Synchronize `stream`, then read and clear the plan's sticky device error
+ * word into *error_bits (MSTAR_DEVERR_* bits; 0 = no error seen).  Returns
+ * INVALID_ARG if a bit was set, OK otherwise, HIP on a runtime failure. */
+int mstar_attn_check(mstar_plan_t* plan, void* stream, int32_t* error_bits);
+
+/* Planner statistics (host side; no device access). */
+int mstar_attn_plan_stats(const mstar_plan_t* plan, mstar_plan_stats* out);
+
+/* Each request's union of visible keys as [lo, hi) pairs into lo_hi[2*num_seqs]
+ * (0, 0 for a request without queries). */
+int mstar_attn_plan_key_ranges(const mstar_plan_t* plan, int32_t* lo_hi, int32_t num_seqs);
+
+/* Copy the host-side work list of one kernel class (0 = multi-row tiles,
+ * 1 = few-row items, 2 = fp32 items, 3 = merge rows) into `items` as int32
+ * records of 8 fields; *count receives the number of records, and at most
+ * `capacity` records are written.  For inspection and tests.
+ * Work record: seq, head (query head; KV head for class 1), row0, nrows,
+ *              key_begin, key_end, partial_slot (-1 = final), 0.
+ * Merge record: packed_row, head, slot0, slot_stride, nslots, 0, 0, 0. */
+int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, int32_t* items,
+                          int64_t capacity, int64_t* count);
+
+/* Release the plan (host and device memory).  The caller guarantees no
+ * enqueued fwd still uses it.  NULL is ignored. */
+void mstar_attn_plan_destroy(mstar_plan_t* plan);
+
+/* Message for the calling thread's last failing call ("" if none). */
+const char* mstar_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MSTAR_ATTN_H */

@@ -1,0 +1,279 @@
+// C-ABI of the attention library: plan construction and upload, fwd launch,
+// device error check and plan introspection.  Nothing here throws across the
+// boundary or aborts; failures return MSTAR_ERR_* with a thread-local message.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "../../include/mstar_attn.h"
+#include "kernels.h"
+#include "planner.h"
+
+#define MSTAR_EXPORT extern "C" __attribute__((visibility("default")))
+
+struct mstar_plan {
+    mstar::HostPlan host;
+    void* dev = nullptr;     // device copy of the plan blob
+    void* pinned = nullptr;  // pinned staging copy (kept until destroy)
+    size_t bytes = 0;
+    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_err = 0;
+    double plan_us = 0.0;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+    g_err = msg;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(MSTAR_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+template <typename T>
+size_t put(unsigned char* blob, size_t off, const std::vector<T>& v) {
+    if (!v.empty()) std::memcpy(blob + off, v.data(), v.size() * sizeof(T));
+    return off;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+}  // namespace
+
+MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
+                                 const mstar_mask_spec* masks, int32_t num_seqs,
+                                 const mstar_segment* segments, int32_t num_segs, void* upload_stream,
+                                 mstar_plan_t** out) {
+    const auto t0 = std::chrono::steady_clock::now();
+    if (!out) return fail(MSTAR_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    if (!params) return fail(MSTAR_ERR_INVALID_ARG, "params is NULL");
+    mstar_attn_params p = *params;
+    const bool host_only = (p.flags & MSTAR_FLAG_HOST_ONLY) != 0;
+    p.flags &= ~MSTAR_FLAG_HOST_ONLY;
+
+    mstar_plan* plan = new (std::nothrow) mstar_plan();
+    if (!plan) return fail(MSTAR_ERR_NOMEM, "host allocation failed");
+    std::string err;
+    int rc;
+    try {
+        rc = mstar::build_host_plan(&p, seqs, masks, num_seqs, segments, num_segs, plan->host, err);
+    } catch (const std::bad_alloc&) {
+        rc = MSTAR_ERR_NOMEM;
+        err = "host allocation failed";
+    } catch (...) {
+        rc = MSTAR_ERR_INVALID_ARG;
+        err = "planner failure";
+    }
+    if (rc != MSTAR_OK) {
+        delete plan;
+        return fail(rc, err);
+    }
+    const mstar::HostPlan& h = plan->host;
+
+    // blob layout: seqs | row_hi | tiles | few | f32 | merges | error word
+    size_t off = 0;
+    plan->off_seqs = off;   off = align256(off + h.seqs.size() * sizeof(mstar::SeqInfo));
+    plan->off_row_hi = off; off = align256(off + h.row_hi.size() * sizeof(int32_t));
+    plan->off_tiles = off;  off = align256(off + h.tiles.size() * sizeof(mstar::WorkItem));
+    plan->off_few = off;    off = align256(off + h.few.size() * sizeof(mstar::WorkItem));
+    plan->off_f32 = off;    off = align256(off + h.f32.size() * sizeof(mstar::WorkItem));
+    plan->off_merge = off;  off = align256(off + h.merges.size() * sizeof(mstar::MergeItem));
+    plan->off_err = off;    off = align256(off + sizeof(int32_t));
+    plan->bytes = off;
+
+    if (!host_only) {
+        hipError_t e = hipHostMalloc(&plan->pinned, plan->bytes, hipHostMallocDefault);
+        if (e != hipSuccess) {
+            delete plan;
+            return hip_fail(e, "hipHostMalloc(plan staging)");
+        }
+        unsigned char* blob = static_cast<unsigned char*>(plan->pinned);
+        std::memset(blob, 0, plan->bytes);
+        put(blob, plan->off_seqs, h.seqs);
+        put(blob, plan->off_row_hi, h.row_hi);
+        put(blob, plan->off_tiles, h.tiles);
+        put(blob, plan->off_few, h.few);
+        put(blob, plan->off_f32, h.f32);
+        put(blob, plan->off_merge, h.merges);
+        e = hipMalloc(&plan->dev, plan->bytes);
+        if (e != hipSuccess) {
+            (void)hipHostFree(plan->pinned);
+            delete plan;
+            return hip_fail(e, "hipMalloc(plan)");
+        }
+        e = hipMemcpyAsync(plan->dev, plan->pinned, plan->bytes, hipMemcpyHostToDevice,
+                           static_cast<hipStream_t>(upload_stream));
+        if (e != hipSuccess) {
+            (void)hipFree(plan->dev);
+            (void)hipHostFree(plan->pinned);
+            delete plan;
+            return hip_fail(e, "plan upload");
+        }
+    }
+    plan->plan_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+    *out = plan;
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan) {
+    if (!plan || plan->host.partial_slots == 0) return 0;
+    const size_t slots = (size_t)plan->host.partial_slots;
+    return align256(slots * plan->host.params.head_dim * sizeof(float)) + align256(slots * sizeof(float));
+}
+
+MSTAR_EXPORT int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const void* k_pages,
+                                const void* v_pages, const int32_t* block_table, void* out, float* lse,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+    if (!plan) return fail(MSTAR_ERR_INVALID_ARG, "plan is NULL");
+    if (!plan->dev) return fail(MSTAR_ERR_INVALID_ARG, "plan was built host-only");
+    const mstar::HostPlan& h = plan->host;
+    const bool any_work = !h.tiles.empty() || !h.few.empty() || !h.f32.empty();
+    if (!any_work) return MSTAR_OK;
+    if (!q || !k_pages || !v_pages || !block_table || !out || !lse)
+        return fail(MSTAR_ERR_INVALID_ARG, "a tensor pointer is NULL");
+    if (!aligned(q, 16) || !aligned(k_pages, 16) || !aligned(v_pages, 16) || !aligned(out, 16) ||
+        !aligned(lse, 4) || !aligned(block_table, 4))
+        return fail(MSTAR_ERR_INVALID_ARG, "q/k_pages/v_pages/out must be 16-byte aligned");
+    const size_t need = mstar_attn_workspace_bytes(plan);
+    if (need > 0 && (!workspace || workspace_bytes < need || !aligned(workspace, 16)))
+        return fail(MSTAR_ERR_WORKSPACE, "workspace missing, misaligned or smaller than mstar_attn_workspace_bytes");
+
+    const int D = h.params.head_dim;
+    unsigned char* blob = static_cast<unsigned char*>(plan->dev);
+    mstar::KArgs a{};
+    a.seqs = reinterpret_cast<const mstar::SeqInfo*>(blob + plan->off_seqs);
+    a.row_hi = reinterpret_cast<const int32_t*>(blob + plan->off_row_hi);
+    a.q = q;
+    a.k = k_pages;
+    a.v = v_pages;
+    a.bt = block_table;
+    a.out = out;
+    a.lse = lse;
+    a.part_o = static_cast<float*>(workspace);
+    a.part_lse = need > 0 ? reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) +
+                                                     align256((size_t)h.partial_slots * D * sizeof(float)))
+                          : nullptr;
+    a.err = reinterpret_cast<int32_t*>(blob + plan->off_err);
+    a.hq = h.params.num_qo_heads;
+    a.hkv = h.params.num_kv_heads;
+    a.group = h.group;
+    a.bt_stride = h.params.max_blocks_per_seq;
+    a.num_pages = h.params.num_pages;
+    a.sm_scale = h.params.sm_scale;
+    a.scale_log2 = h.params.sm_scale * 1.4426950408889634f;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    hipError_t e;
+    if (!h.tiles.empty()) {
+        a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_tiles);
+        a.n_items = (int32_t)h.tiles.size();
+        if ((e = mstar::launch_tiles(a, D, s)) != hipSuccess) return hip_fail(e, "tile kernel launch");
+    }
+    if (!h.few.empty()) {
+        a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_few);
+        a.n_items = (int32_t)h.few.size();
+        if ((e = mstar::launch_few(a, D, h.decode_rb, s)) != hipSuccess) return hip_fail(e, "few-row kernel launch");
+    }
+    if (!h.f32.empty()) {
+        a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_f32);
+        a.n_items = (int32_t)h.f32.size();
+        if ((e = mstar::launch_f32(a, D, s)) != hipSuccess) return hip_fail(e, "fp32 kernel launch");
+    }
+    if (!h.merges.empty()) {
+        mstar::MArgs m{};
+        m.items = reinterpret_cast<const mstar::MergeItem*>(blob + plan->off_merge);
+        m.part_o = a.part_o;
+        m.part_lse = a.part_lse;
+        m.out = out;
+        m.lse = lse;
+        m.n_items = (int32_t)h.merges.size();
+        m.hq = a.hq;
+        if ((e = mstar::launch_merge(m, D, h.params.dtype == MSTAR_DTYPE_BF16, s)) != hipSuccess)
+            return hip_fail(e, "merge kernel launch");
+    }
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_attn_check(mstar_plan_t* plan, void* stream, int32_t* error_bits) {
+    if (!plan || !error_bits) return fail(MSTAR_ERR_INVALID_ARG, "plan or error_bits is NULL");
+    *error_bits = 0;
+    if (!plan->dev) return MSTAR_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    int32_t* d_err = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(plan->dev) + plan->off_err);
+    int32_t v = 0;
+    e = hipMemcpy(&v, d_err, sizeof v, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "error word read");
+    *error_bits = v;
+    if (v != 0) {
+        const int32_t zero = 0;
+        e = hipMemcpy(d_err, &zero, sizeof zero, hipMemcpyHostToDevice);
+        if (e != hipSuccess) return hip_fail(e, "error word clear");
+        return fail(MSTAR_ERR_INVALID_ARG, "a block-table entry was outside [0, num_pages)");
+    }
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_attn_plan_stats(const mstar_plan_t* plan, mstar_plan_stats* out) {
+    if (!plan || !out) return fail(MSTAR_ERR_INVALID_ARG, "plan or out is NULL");
+    const mstar::HostPlan& h = plan->host;
+    out->visible_pairs = h.visible_pairs;
+    out->prefill_items = (int64_t)h.tiles.size();
+    out->decode_items = (int64_t)h.few.size();
+    out->f32_items = (int64_t)h.f32.size();
+    out->merge_rows = (int64_t)h.merges.size();
+    out->partial_slots = h.partial_slots;
+    out->total_q = h.total_q;
+    out->plan_host_us = plan->plan_us;
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_attn_plan_key_ranges(const mstar_plan_t* plan, int32_t* lo_hi, int32_t num_seqs) {
+    if (!plan || (!lo_hi && num_seqs > 0)) return fail(MSTAR_ERR_INVALID_ARG, "plan or lo_hi is NULL");
+    if (num_seqs != plan->host.num_seqs) return fail(MSTAR_ERR_INVALID_ARG, "num_seqs differs from the plan");
+    for (int32_t r = 0; r < num_seqs; ++r) {
+        lo_hi[2 * r] = plan->host.key_lo[r];
+        lo_hi[2 * r + 1] = plan->host.key_hi[r];
+    }
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, int32_t* items, int64_t capacity,
+                                       int64_t* count) {
+    if (!plan || !count) return fail(MSTAR_ERR_INVALID_ARG, "plan or count is NULL");
+    const mstar::HostPlan& h = plan->host;
+    const void* src;
+    size_t n;
+    switch (kind) {
+        case 0: src = h.tiles.data(); n = h.tiles.size(); break;
+        case 1: src = h.few.data(); n = h.few.size(); break;
+        case 2: src = h.f32.data(); n = h.f32.size(); break;
+        case 3: src = h.merges.data(); n = h.merges.size(); break;
+        default: return fail(MSTAR_ERR_INVALID_ARG, "kind must be 0..3");
+    }
+    *count = (int64_t)n;
+    if (capacity > 0 && !items) return fail(MSTAR_ERR_INVALID_ARG, "items is NULL");
+    const size_t m = capacity < 0 ? 0 : std::min<size_t>(n, (size_t)capacity);
+    if (m) std::memcpy(items, src, m * 32);
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT void mstar_attn_plan_destroy(mstar_plan_t* plan) {
+    if (!plan) return;
+    if (plan->dev) (void)hipFree(plan->dev);
+    if (plan->pinned) (void)hipHostFree(plan->pinned);
+    delete plan;
+}
+
+MSTAR_EXPORT const char* mstar_last_error(void) { return g_err.c_str(); }

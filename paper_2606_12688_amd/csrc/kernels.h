@@ -1,0 +1,44 @@
+// Launch interface between the C-ABI layer and the HIP kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "plan_types.h"
+
+namespace mstar {
+
+struct KArgs {
+    const SeqInfo* seqs;
+    const int32_t* row_hi;
+    const WorkItem* items;
+    const void* q;
+    const void* k;
+    const void* v;
+    const int32_t* bt;
+    void* out;
+    float* lse;
+    float* part_o;    // [partial_slots][head_dim] fp32
+    float* part_lse;  // [partial_slots] fp32 natural log
+    int32_t* err;     // sticky device error word
+    int32_t n_items;
+    int32_t hq, hkv, group, bt_stride, num_pages;
+    float sm_scale;
+    float scale_log2;  // sm_scale * log2(e)
+};
+
+struct MArgs {
+    const MergeItem* items;
+    const float* part_o;
+    const float* part_lse;
+    void* out;
+    float* lse;
+    int32_t n_items;
+    int32_t hq;
+};
+
+hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_few(const KArgs& a, int head_dim, int row_blocks, hipStream_t s);
+hipError_t launch_f32(const KArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_merge(const MArgs& a, int head_dim, bool bf16_out, hipStream_t s);
+
+}  // namespace mstar

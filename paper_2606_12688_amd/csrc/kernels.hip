@@ -1,0 +1,683 @@
+// HIP kernels for batched paged attention with per-row visible intervals,
+// written for gfx950 (CDNA4): 64-lane waves, 16x16x32 bf16 MFMA, LDS
+// transpose reads.
+//
+// Notation used throughout: a 16x16x32 MFMA computes D[16][16] += A[16][32] *
+// B[32][16].  Lane l (group G = l / 16, index n = l % 16) supplies
+// A[n][8G .. 8G+7] and B[8G .. 8G+7][n], and receives D[4G .. 4G+3][n].
+//
+// Scores are formed transposed, S^T = K * Q^T (A = 16 keys x 32 dims of K,
+// B = 32 dims x 16 query rows of Q^T), so lane l owns query row n and keys
+// 4G .. 4G+3 of every 16-key block.  The weighted value sum is likewise
+// transposed, O^T = V^T * P^T: the B operand P^T needs exactly the score
+// values lane l already holds (two 16-key blocks make one 32-key step), and the
+// A operand V^T is read from LDS with ds_read_b64_tr_b16.  Row statistics
+// (running max, running sum, rescale factor) are therefore per-lane scalars.
+//
+// The softmax runs in base 2: s2 = s * sm_scale * log2(e), p = 2^(s2 - m2),
+// and lse = (m2 + log2 l) * ln 2 at the end.
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace mstar {
+namespace {
+
+typedef __bf16 bf16_t;
+typedef bf16_t bf16x8 __attribute__((ext_vector_type(8)));
+typedef bf16_t bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kNegInf = -__builtin_inff();
+
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Reductions over the four lanes l, l^16, l^32, l^48 that share a query row.
+__device__ __forceinline__ float rowgroup_max(float x) {
+    x = fmaxf(x, __shfl_xor(x, 16, 64));
+    x = fmaxf(x, __shfl_xor(x, 32, 64));
+    return x;
+}
+__device__ __forceinline__ float rowgroup_sum(float x) {
+    x += __shfl_xor(x, 16, 64);
+    x += __shfl_xor(x, 32, 64);
+    return x;
+}
+
+__device__ __forceinline__ bf16x4 lds_read_tr16(const bf16_t* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
+}
+
+__device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
+    return bf16x8{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+
+__device__ __forceinline__ bf16x8 to_bf16x8(f32x4 a, f32x4 b) {
+    return cat(__builtin_convertvector(a, bf16x4), __builtin_convertvector(b, bf16x4));
+}
+
+// Element offset of key t of KV head kvh, or -1 if its block-table entry is
+// outside the pool (recorded in the sticky error word; the key reads as 0).
+__device__ __forceinline__ int64_t kv_offset(const KArgs& a, const int32_t* bt_row, int32_t t,
+                                             int32_t kvh, int D) {
+    const int32_t page = bt_row[t >> 4];
+    if ((uint32_t)page >= (uint32_t)a.num_pages) {
+        atomicOr(a.err, 1);
+        return -1;
+    }
+    return (((int64_t)page * 16 + (t & 15)) * a.hkv + kvh) * D;
+}
+
+__device__ __forceinline__ uint4 load16(const void* base, int64_t elem_off_bf16) {
+    return *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(base) + elem_off_bf16);
+}
+
+// Visible interval of query row i of a request, clipped to the item's keys.
+__device__ __forceinline__ void row_interval(const KArgs& a, const SeqInfo& si, const WorkItem& it,
+                                             int32_t i, int32_t& lo, int32_t& hi) {
+    const int32_t pos = si.kv_len - si.q_len + i;
+    int32_t l0 = si.window > 0 ? max(0, pos - si.window + 1) : 0;
+    int32_t h0 = a.row_hi[si.hi_off + i];
+    lo = max(l0, it.k_begin);
+    hi = min(h0, it.k_end);
+}
+
+// Online-softmax update of one 16-row block with NB 16-key blocks of scores
+// (already scaled to base 2 and masked).  Returns the rescale factor for O.
+template <int NB>
+__device__ __forceinline__ float softmax_update(f32x4 (&s)[NB], float& m, float& l) {
+    float mx = kNegInf;
+#pragma unroll
+    for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kb][i]);
+    mx = rowgroup_max(mx);
+    const float m_new = fmaxf(m, mx);
+    const float m_use = m_new == kNegInf ? 0.0f : m_new;
+    const float alpha = fast_exp2(m - m_use);
+    float sum = 0.0f;
+#pragma unroll
+    for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float p = fast_exp2(s[kb][i] - m_use);
+            s[kb][i] = p;
+            sum += p;
+        }
+    l = l * alpha + sum;  // per-lane partial sum; the row total is reduced at the end
+    m = m_new;
+    return alpha;
+}
+
+// ---------------------------------------------------------------------------
+// Multi-row tile kernel: one workgroup = 128 query rows of one query head
+// (4 waves x 2 blocks of 16 rows) against the item's key range, 64 keys per
+// LDS tile, K and V tiles double-buffered in LDS.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
+    constexpr int BN = kTileKeys;
+    constexpr int KS = D + 8;   // K row stride in LDS: 16-byte skew per row
+    constexpr int VS = D + 16;  // V row stride in LDS: 32-byte skew per row
+    constexpr int DS = D / 32;  // MFMA steps over the head dimension
+    constexpr int DB = D / 16;  // 16-wide blocks of O^T
+    constexpr int CH = D / 8;   // 16-byte chunks per key row
+    constexpr int LOADS = BN * CH / 256;
+    __shared__ __attribute__((aligned(16))) bf16_t k_lds[2][BN * KS];
+    __shared__ __attribute__((aligned(16))) bf16_t v_lds[2][BN * VS];
+
+    const WorkItem it = a.items[blockIdx.x];
+    const SeqInfo si = a.seqs[it.seq];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int n = lane & 15, grp = lane >> 4;
+    const int kvh = it.head / a.group;
+    const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
+
+    // ---- rows owned by this lane ------------------------------------------
+    int32_t lo[2], hi[2];
+    bool valid[2];
+    bf16x8 qf[2][DS];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+        const int r = wave * 32 + rb * 16 + n;
+        valid[rb] = r < it.nrows;
+        lo[rb] = 0;
+        hi[rb] = 0;
+        if (valid[rb]) row_interval(a, si, it, it.row0 + r, lo[rb], hi[rb]);
+        const int64_t qoff = ((int64_t)(si.q_start + it.row0 + r) * a.hq + it.head) * D;
+#pragma unroll
+        for (int s = 0; s < DS; ++s) {
+            if (valid[rb]) {
+                uint4 u = load16(a.q, qoff + 32 * s + 8 * grp);
+                qf[rb][s] = __builtin_bit_cast(bf16x8, u);
+            } else {
+                qf[rb][s] = bf16x8{};
+            }
+        }
+    }
+    // wave-uniform bounds: intervals never shrink from one row to the next
+    const int wr0 = wave * 32;
+    const int wr1 = min(wave * 32 + 31, it.nrows - 1);
+    const bool wave_active = wr0 < it.nrows;
+    int32_t w_lo_min = 0, w_lo_max = 0, w_hi_min = 0, w_hi_max = 0;
+    if (wave_active) {
+        row_interval(a, si, it, it.row0 + wr0, w_lo_min, w_hi_min);
+        row_interval(a, si, it, it.row0 + wr1, w_lo_max, w_hi_max);
+    }
+
+    float m[2] = {kNegInf, kNegInf}, l[2] = {0.0f, 0.0f};
+    f32x4 o[2][DB];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[rb][db] = f32x4{0, 0, 0, 0};
+
+    uint4 kreg[LOADS], vreg[LOADS];
+    auto load_tile = [&](int32_t k0) {
+#pragma unroll
+        for (int j = 0; j < LOADS; ++j) {
+            const int c = tid + 256 * j;
+            const int row = c / CH, col = (c % CH) * 8;
+            const int32_t t = k0 + row;
+            kreg[j] = uint4{0, 0, 0, 0};
+            vreg[j] = uint4{0, 0, 0, 0};
+            if (t < it.k_end) {
+                const int64_t off = kv_offset(a, bt_row, t, kvh, D);
+                if (off >= 0) {
+                    kreg[j] = load16(a.k, off + col);
+                    vreg[j] = load16(a.v, off + col);
+                }
+            }
+        }
+    };
+    auto store_tile = [&](int buf) {
+#pragma unroll
+        for (int j = 0; j < LOADS; ++j) {
+            const int c = tid + 256 * j;
+            const int row = c / CH, col = (c % CH) * 8;
+            *reinterpret_cast<uint4*>(&k_lds[buf][row * KS + col]) = kreg[j];
+            *reinterpret_cast<uint4*>(&v_lds[buf][row * VS + col]) = vreg[j];
+        }
+    };
+
+    const int n_tiles = (it.k_end - it.k_begin + BN - 1) / BN;
+    load_tile(it.k_begin);
+    store_tile(0);
+    __syncthreads();
+
+    for (int tix = 0; tix < n_tiles; ++tix) {
+        const int32_t k0 = it.k_begin + tix * BN;
+        const int buf = tix & 1;
+        const bool more = tix + 1 < n_tiles;
+        if (more) load_tile(k0 + BN);
+
+        if (wave_active && k0 < w_hi_max && k0 + BN > w_lo_min) {
+            const bool full = k0 >= w_lo_max && k0 + BN <= w_hi_min;
+            f32x4 sc[2][4];
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb) sc[rb][kb] = f32x4{0, 0, 0, 0};
+#pragma unroll
+            for (int kb = 0; kb < 4; ++kb) {
+#pragma unroll
+                for (int s = 0; s < DS; ++s) {
+                    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
+                        &k_lds[buf][(kb * 16 + n) * KS + 32 * s + 8 * grp]);
+#pragma unroll
+                    for (int rb = 0; rb < 2; ++rb) sc[rb][kb] = mfma16(kf, qf[rb][s], sc[rb][kb]);
+                }
+            }
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb) {
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int32_t key = k0 + kb * 16 + 4 * grp + i;
+                        float x = sc[rb][kb][i] * a.scale_log2;
+                        if (!full && !(key >= lo[rb] && key < hi[rb])) x = kNegInf;
+                        sc[rb][kb][i] = x;
+                    }
+                const float alpha = softmax_update<4>(sc[rb], m[rb], l[rb]);
+#pragma unroll
+                for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+            }
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                bf16x8 pf[2];
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb) pf[rb] = to_bf16x8(sc[rb][2 * c], sc[rb][2 * c + 1]);
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const bf16_t* base = &v_lds[buf][(32 * c + 4 * grp + (n >> 2)) * VS + db * 16 + (n & 3) * 4];
+                    const bf16x8 vf = cat(lds_read_tr16(base), lds_read_tr16(base + 16 * VS));
+#pragma unroll
+                    for (int rb = 0; rb < 2; ++rb) o[rb][db] = mfma16(vf, pf[rb], o[rb][db]);
+                }
+            }
+        }
+        if (more) store_tile(buf ^ 1);
+        __syncthreads();
+    }
+
+    // ---- epilogue -------------------------------------------------------------
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+        const float lt = rowgroup_sum(l[rb]);
+        if (!valid[rb]) continue;
+        const int r = wave * 32 + rb * 16 + n;
+        const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
+        const float lse = lt > 0.0f ? (m[rb] + __log2f(lt)) * kLn2 : kNegInf;
+        if (it.part < 0) {
+            const int64_t row = (int64_t)(si.q_start + it.row0 + r) * a.hq + it.head;
+            bf16_t* out = reinterpret_cast<bf16_t*>(a.out) + row * D;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const bf16x4 v = __builtin_convertvector(o[rb][db] * inv, bf16x4);
+                *reinterpret_cast<bf16x4*>(out + db * 16 + 4 * grp) = v;
+            }
+            if (grp == 0) a.lse[row] = lse;
+        } else {
+            const int64_t slot = it.part + r;
+            float* po = a.part_o + slot * D;
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+                *reinterpret_cast<f32x4*>(po + db * 16 + 4 * grp) = o[rb][db] * inv;
+            if (grp == 0) a.part_lse[slot] = lse;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Few-row kernel: one workgroup = up to 16*RB rows (query rows x the query
+// heads of one KV head) against the item's key range.  The four waves take
+// interleaved 32-key steps; K goes straight from HBM into MFMA operand
+// registers, V is staged through a wave-private LDS slice for the transpose
+// read, and the next step's loads are in flight while the current one is
+// computed.  The four waves' partial results are combined through LDS.
+// ---------------------------------------------------------------------------
+template <int D, int RB>
+__global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(KArgs a) {
+    constexpr int SK = kSubKeys;
+    constexpr int VS = D + 16;
+    constexpr int DS = D / 32, DB = D / 16, CH = D / 8;
+    constexpr int VL = SK * CH / 64;  // 16-byte V chunks per lane per step
+    static_assert(RB * 16 * D * 4 <= 4 * SK * VS * 2, "combine buffer must fit in the V staging area");
+    __shared__ __attribute__((aligned(16))) bf16_t v_lds[4][SK * VS];
+    __shared__ float ml_lds[4][2][RB * 16];
+    __shared__ float fin_lds[2][RB * 16];
+
+    const WorkItem it = a.items[blockIdx.x];
+    const SeqInfo si = a.seqs[it.seq];
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int n = lane & 15, grp = lane >> 4;
+    const int G = a.group;
+    const int kvh = it.head;
+    const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
+
+    int32_t lo[RB], hi[RB];
+    bool valid[RB];
+    bf16x8 qf[RB][DS];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const int r = rb * 16 + n;
+        valid[rb] = r < it.nrows;
+        const int rr = it.row0 + r;
+        const int qi = rr / G, h = kvh * G + rr % G;
+        lo[rb] = 0;
+        hi[rb] = 0;
+        if (valid[rb]) row_interval(a, si, it, qi, lo[rb], hi[rb]);
+        const int64_t qoff = ((int64_t)(si.q_start + qi) * a.hq + h) * D;
+#pragma unroll
+        for (int s = 0; s < DS; ++s) {
+            if (valid[rb]) {
+                qf[rb][s] = __builtin_bit_cast(bf16x8, load16(a.q, qoff + 32 * s + 8 * grp));
+            } else {
+                qf[rb][s] = bf16x8{};
+            }
+        }
+    }
+    int32_t lo_max, hi_min, dummy;
+    {
+        const int q_first = it.row0 / G, q_last = (it.row0 + it.nrows - 1) / G;
+        row_interval(a, si, it, q_first, dummy, hi_min);
+        row_interval(a, si, it, q_last, lo_max, dummy);
+    }
+
+    float m[RB], l[RB];
+    f32x4 o[RB][DB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        m[rb] = kNegInf;
+        l[rb] = 0.0f;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[rb][db] = f32x4{0, 0, 0, 0};
+    }
+
+    struct Step {
+        uint4 k[2][DS];
+        uint4 v[VL];
+    };
+    auto load_step = [&](Step& st, int32_t k0) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            const int32_t t = k0 + kb * 16 + n;
+            int64_t off = -1;
+            if (t < it.k_end) off = kv_offset(a, bt_row, t, kvh, D);
+#pragma unroll
+            for (int s = 0; s < DS; ++s)
+                st.k[kb][s] = off >= 0 ? load16(a.k, off + 32 * s + 8 * grp) : uint4{0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int j = 0; j < VL; ++j) {
+            const int c = lane + 64 * j;
+            const int row = c / CH, col = (c % CH) * 8;
+            const int32_t t = k0 + row;
+            int64_t off = -1;
+            if (t < it.k_end) off = kv_offset(a, bt_row, t, kvh, D);
+            st.v[j] = off >= 0 ? load16(a.v, off + col) : uint4{0, 0, 0, 0};
+        }
+    };
+
+    bf16_t* vst = v_lds[wave];
+    const int n_steps = (it.k_end - it.k_begin + SK - 1) / SK;
+    Step cur, nxt;
+    if (wave < n_steps) load_step(cur, it.k_begin + wave * SK);
+    for (int st = wave; st < n_steps; st += 4) {
+        const int32_t k0 = it.k_begin + st * SK;
+        const bool more = st + 4 < n_steps;
+        if (more) load_step(nxt, k0 + 4 * SK);
+
+        f32x4 sc[RB][2];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) sc[rb][0] = sc[rb][1] = f32x4{0, 0, 0, 0};
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int s = 0; s < DS; ++s) {
+                const bf16x8 kf = __builtin_bit_cast(bf16x8, cur.k[kb][s]);
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb) sc[rb][kb] = mfma16(kf, qf[rb][s], sc[rb][kb]);
+            }
+        // stage V for the transpose read (wave-private slice; LDS executes a
+        // wave's accesses in order, the asm keeps the compiler from reordering)
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int j = 0; j < VL; ++j) {
+            const int c = lane + 64 * j;
+            const int row = c / CH, col = (c % CH) * 8;
+            *reinterpret_cast<uint4*>(&vst[row * VS + col]) = cur.v[j];
+        }
+        asm volatile("" ::: "memory");
+
+        const bool full = k0 >= lo_max && k0 + SK <= hi_min;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int32_t key = k0 + kb * 16 + 4 * grp + i;
+                    float x = sc[rb][kb][i] * a.scale_log2;
+                    if (!full && !(key >= lo[rb] && key < hi[rb])) x = kNegInf;
+                    sc[rb][kb][i] = x;
+                }
+            const float alpha = softmax_update<2>(sc[rb], m[rb], l[rb]);
+#pragma unroll
+            for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+        }
+        bf16x8 pf[RB];
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) pf[rb] = to_bf16x8(sc[rb][0], sc[rb][1]);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+            const bf16_t* base = &vst[(4 * grp + (n >> 2)) * VS + db * 16 + (n & 3) * 4];
+            const bf16x8 vf = cat(lds_read_tr16(base), lds_read_tr16(base + 16 * VS));
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb) o[rb][db] = mfma16(vf, pf[rb], o[rb][db]);
+        }
+        asm volatile("" ::: "memory");
+        if (more) cur = nxt;
+    }
+
+    // ---- combine the four waves -------------------------------------------------
+    float lt[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) lt[rb] = rowgroup_sum(l[rb]);
+    __syncthreads();  // every wave is done with its V slice
+    if (grp == 0) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+            ml_lds[wave][0][rb * 16 + n] = m[rb];
+            ml_lds[wave][1][rb * 16 + n] = lt[rb];
+        }
+    }
+    __syncthreads();
+    float* obuf = reinterpret_cast<float*>(&v_lds[0][0]);
+    float scale_own[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const int row = rb * 16 + n;
+        float mstar = kNegInf;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) mstar = fmaxf(mstar, ml_lds[w][0][row]);
+        const float mu = mstar == kNegInf ? 0.0f : mstar;
+        float L = 0.0f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) L += fast_exp2(ml_lds[w][0][row] - mu) * ml_lds[w][1][row];
+        scale_own[rb] = fast_exp2(m[rb] - mu);
+        if (wave == 0 && grp == 0) {
+            fin_lds[0][row] = mstar;
+            fin_lds[1][row] = L;
+        }
+    }
+    for (int w = 0; w < 4; ++w) {
+        if (wave == w) {
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    f32x4* dst = reinterpret_cast<f32x4*>(&obuf[(rb * 16 + n) * D + db * 16 + 4 * grp]);
+                    const f32x4 val = o[rb][db] * scale_own[rb];
+                    *dst = (w == 0) ? val : *dst + val;
+                }
+        }
+        __syncthreads();
+    }
+    constexpr int NV = RB * 16 * D / 4;  // float4 elements of the combined block
+    for (int e = tid; e < NV; e += 256) {
+        const int row = e / (D / 4), d4 = (e % (D / 4)) * 4;
+        if (row >= it.nrows) continue;
+        const float mstar = fin_lds[0][row], L = fin_lds[1][row];
+        const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+        const float lse = L > 0.0f ? (mstar + __log2f(L)) * kLn2 : kNegInf;
+        const f32x4 val = *reinterpret_cast<const f32x4*>(&obuf[row * D + d4]) * inv;
+        const int rr = it.row0 + row;
+        if (it.part < 0) {
+            const int64_t orow = (int64_t)(si.q_start + rr / G) * a.hq + kvh * G + rr % G;
+            *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16_t*>(a.out) + orow * D + d4) =
+                __builtin_convertvector(val, bf16x4);
+            if (d4 == 0) a.lse[orow] = lse;
+        } else {
+            const int64_t slot = it.part + row;
+            *reinterpret_cast<f32x4*>(a.part_o + slot * D + d4) = val;
+            if (d4 == 0) a.part_lse[slot] = lse;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 kernel: one wave per (query row, head); lanes take 64 keys at a time
+// for the scores and the head dimension for the weighted value sum.  All
+// arithmetic in fp32 with the accurate exp/log.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void f32_kernel(KArgs a) {
+    constexpr int E = D / 64;
+    __shared__ float q_lds[4][D];
+    const WorkItem it = a.items[blockIdx.x];
+    const SeqInfo si = a.seqs[it.seq];
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int r = wave;
+    if (r >= it.nrows) return;
+    const int i = it.row0 + r;
+    int32_t lo, hi;
+    row_interval(a, si, it, i, lo, hi);
+    const int kvh = it.head / a.group;
+    const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
+    const float* qg = reinterpret_cast<const float*>(a.q) + ((int64_t)(si.q_start + i) * a.hq + it.head) * D;
+    const float* kg = reinterpret_cast<const float*>(a.k);
+    const float* vg = reinterpret_cast<const float*>(a.v);
+#pragma unroll
+    for (int e = 0; e < E; ++e) q_lds[wave][lane + 64 * e] = qg[lane + 64 * e];
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_wave_barrier();
+
+    float m = kNegInf, l = 0.0f, acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+    for (int32_t kb = lo; kb < hi; kb += 64) {
+        const int32_t t = kb + lane;
+        float s = kNegInf;
+        if (t < hi) {
+            const int32_t page = bt_row[t >> 4];
+            if ((uint32_t)page < (uint32_t)a.num_pages) {
+                const float* kr = kg + (((int64_t)page * 16 + (t & 15)) * a.hkv + kvh) * D;
+                float dot = 0.0f;
+                for (int d = 0; d < D; d += 4) {
+                    const float4 kv = *reinterpret_cast<const float4*>(kr + d);
+                    dot = fmaf(q_lds[wave][d], kv.x, dot);
+                    dot = fmaf(q_lds[wave][d + 1], kv.y, dot);
+                    dot = fmaf(q_lds[wave][d + 2], kv.z, dot);
+                    dot = fmaf(q_lds[wave][d + 3], kv.w, dot);
+                }
+                s = dot * a.sm_scale;
+            } else {
+                atomicOr(a.err, 1);
+                s = 0.0f;  // the key reads as zeros
+            }
+        }
+        float cm = s;
+        for (int off = 32; off > 0; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off, 64));
+        const float m_new = fmaxf(m, cm);
+        const float alpha = m == kNegInf ? 0.0f : expf(m - m_new);
+        const float p = t < hi ? expf(s - m_new) : 0.0f;
+        float ps = p;
+        for (int off = 32; off > 0; off >>= 1) ps += __shfl_xor(ps, off, 64);
+        l = l * alpha + ps;
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] *= alpha;
+        const int nk = min(64, hi - kb);
+        for (int j = 0; j < nk; ++j) {
+            const float pj = __shfl(p, j, 64);
+            const int32_t tj = kb + j;
+            const int32_t page = bt_row[tj >> 4];
+            if ((uint32_t)page >= (uint32_t)a.num_pages) continue;
+            const float* vr = vg + (((int64_t)page * 16 + (tj & 15)) * a.hkv + kvh) * D;
+#pragma unroll
+            for (int e = 0; e < E; ++e) acc[e] = fmaf(pj, vr[lane + 64 * e], acc[e]);
+        }
+        m = m_new;
+    }
+    const int64_t row = (int64_t)(si.q_start + i) * a.hq + it.head;
+    float* out = reinterpret_cast<float*>(a.out) + row * D;
+    const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) out[lane + 64 * e] = acc[e] * inv;
+    if (lane == 0) a.lse[row] = l > 0.0f ? m + logf(l) : kNegInf;
+}
+
+// ---------------------------------------------------------------------------
+// Merge kernel: one wave per (row, head); combines the partial results of
+// split key ranges by their log-sum-exps (lanes over the head dimension).
+// ---------------------------------------------------------------------------
+template <int D, bool BF16>
+__global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
+    constexpr int E = D / 64;
+    const int idx = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (idx >= a.n_items) return;
+    const MergeItem mi = a.items[idx];
+    float mstar = kNegInf;
+    for (int s = 0; s < mi.nslots; ++s) mstar = fmaxf(mstar, a.part_lse[mi.slot0 + (int64_t)s * mi.stride]);
+    float acc[E], tot = 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+    if (mstar != kNegInf) {
+        for (int s = 0; s < mi.nslots; ++s) {
+            const int64_t slot = mi.slot0 + (int64_t)s * mi.stride;
+            const float w = expf(a.part_lse[slot] - mstar);
+            tot += w;
+#pragma unroll
+            for (int e = 0; e < E; ++e) acc[e] = fmaf(w, a.part_o[slot * D + lane + 64 * e], acc[e]);
+        }
+    }
+    const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
+    const int64_t row = (int64_t)mi.row * a.hq + mi.head;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const float v = acc[e] * inv;
+        if (BF16)
+            reinterpret_cast<bf16_t*>(a.out)[row * D + lane + 64 * e] = (bf16_t)v;
+        else
+            reinterpret_cast<float*>(a.out)[row * D + lane + 64 * e] = v;
+    }
+    if (lane == 0) a.lse[row] = tot > 0.0f ? mstar + logf(tot) : kNegInf;
+}
+
+}  // namespace
+
+hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s) {
+    if (a.n_items == 0) return hipSuccess;
+    if (head_dim == 64)
+        hipLaunchKernelGGL(tile_kernel<64>, dim3(a.n_items), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(tile_kernel<128>, dim3(a.n_items), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_few(const KArgs& a, int head_dim, int rb, hipStream_t s) {
+    if (a.n_items == 0) return hipSuccess;
+    const dim3 g(a.n_items), b(256);
+    if (head_dim == 64) {
+        if (rb == 1) hipLaunchKernelGGL((few_kernel<64, 1>), g, b, 0, s, a);
+        else if (rb == 2) hipLaunchKernelGGL((few_kernel<64, 2>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((few_kernel<64, 4>), g, b, 0, s, a);
+    } else {
+        if (rb == 1) hipLaunchKernelGGL((few_kernel<128, 1>), g, b, 0, s, a);
+        else if (rb == 2) hipLaunchKernelGGL((few_kernel<128, 2>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((few_kernel<128, 4>), g, b, 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_f32(const KArgs& a, int head_dim, hipStream_t s) {
+    if (a.n_items == 0) return hipSuccess;
+    if (head_dim == 64)
+        hipLaunchKernelGGL(f32_kernel<64>, dim3(a.n_items), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(f32_kernel<128>, dim3(a.n_items), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_merge(const MArgs& a, int head_dim, bool bf16_out, hipStream_t s) {
+    if (a.n_items == 0) return hipSuccess;
+    const dim3 g((a.n_items + 3) / 4), b(256);
+    if (head_dim == 64) {
+        if (bf16_out) hipLaunchKernelGGL((merge_kernel<64, true>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((merge_kernel<64, false>), g, b, 0, s, a);
+    } else {
+        if (bf16_out) hipLaunchKernelGGL((merge_kernel<128, true>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((merge_kernel<128, false>), g, b, 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace mstar

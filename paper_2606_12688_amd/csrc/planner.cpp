@@ -1,0 +1,332 @@
+// Host planner for batched paged attention with per-request segment masks.
+//
+// The paper's workers build the attention plan for the next batch on a side
+// thread while the current batch runs, and name plan construction as the
+// heaviest CPU overhead of a step (Sec. 3.3, Runtime).  This planner therefore
+// reads only descriptors (never tensor data), is re-entrant, and does work
+// linear in the number of query rows.
+//
+// Steps:
+//  1. validate descriptors;
+//  2. turn each request's segments + window into one visible key interval
+//     [lo, hi) per query row (block ids never decrease along a request, so a
+//     row sees every key up to the end of its own block, and a window only
+//     cuts keys off from below);
+//  3. cut the batch into work items: few-row items (decode-like requests whose
+//     query rows times grouped heads fit one 64-row item; all query heads of a
+//     KV head share one stream of K/V) and 128-row tiles of one query head for
+//     everything else;
+//  4. split key ranges into chunks when there are too few items to fill the
+//     GPU (partials are merged by their log-sum-exps afterwards);
+//  5. order every list longest first so that the hardware dispatcher, which
+//     starts workgroups in order as slots free up, ends with short items.
+#include "planner.h"
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstdio>
+
+namespace mstar {
+namespace {
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+struct RowIntervals {
+    std::vector<int32_t> lo, hi;
+};
+
+// Visible interval of every query row of one request.  Returns false (with a
+// message) if the segments do not tile [0, kv_len) in order.
+bool row_intervals(const mstar_seq_desc& s, const mstar_mask_spec& m, const mstar_segment* segs,
+                   RowIntervals& out, std::string& err) {
+    // validate the tiling first
+    int64_t pos = 0;
+    for (int32_t k = 0; k < m.seg_count; ++k) {
+        const mstar_segment& g = segs[m.seg_begin + k];
+        if (g.start != pos || g.len < 0) {
+            err = "segments must tile [0, kv_len) in order";
+            return false;
+        }
+        if (g.kind != MSTAR_SEG_CAUSAL && g.kind != MSTAR_SEG_FULL && g.kind != MSTAR_SEG_BLOCKS) {
+            err = "unknown segment kind";
+            return false;
+        }
+        if (g.kind == MSTAR_SEG_BLOCKS && g.block <= 0) {
+            err = "BLOCKS segment needs block > 0";
+            return false;
+        }
+        pos += g.len;
+    }
+    if (pos != s.kv_len) {
+        err = "segments must tile [0, kv_len) in order";
+        return false;
+    }
+    out.lo.resize(s.q_len);
+    out.hi.resize(s.q_len);
+    int32_t k = 0;
+    for (int32_t i = 0; i < s.q_len; ++i) {
+        const int64_t p = (int64_t)s.kv_len - s.q_len + i;
+        while (k < m.seg_count) {
+            const mstar_segment& g = segs[m.seg_begin + k];
+            if (p < (int64_t)g.start + g.len) break;
+            ++k;
+        }
+        const mstar_segment& g = segs[m.seg_begin + k];  // p lies inside g
+        const int64_t seg_end = (int64_t)g.start + g.len;
+        int64_t hi;
+        if (g.kind == MSTAR_SEG_CAUSAL) {
+            hi = p + 1;
+        } else if (g.kind == MSTAR_SEG_FULL) {
+            hi = seg_end;
+        } else {
+            hi = std::min<int64_t>(g.start + ((p - g.start) / g.block + 1) * (int64_t)g.block, seg_end);
+        }
+        const int64_t lo = m.window > 0 ? std::max<int64_t>(0, p - m.window + 1) : 0;
+        out.lo[i] = (int32_t)lo;
+        out.hi[i] = (int32_t)hi;
+    }
+    return true;
+}
+
+int32_t align_down16(int32_t x) { return x & ~(kPage - 1); }
+
+struct Unit {  // a few-row unit or a tile before key splitting
+    int32_t seq, head, row0, nrows, k_begin, k_end;
+    int64_t cost;
+};
+
+}  // namespace
+
+int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
+                    const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segs,
+                    int32_t num_segs, HostPlan& plan, std::string& err) {
+    if (!params) { err = "params is NULL"; return MSTAR_ERR_INVALID_ARG; }
+    if (num_seqs < 0 || num_segs < 0) { err = "negative count"; return MSTAR_ERR_INVALID_ARG; }
+    if (num_seqs > 0 && (!seqs || !masks)) { err = "seqs/masks is NULL"; return MSTAR_ERR_INVALID_ARG; }
+    if (num_segs > 0 && !segs) { err = "segments is NULL"; return MSTAR_ERR_INVALID_ARG; }
+    const mstar_attn_params& P = *params;
+    if (P.num_qo_heads <= 0 || P.num_kv_heads <= 0 || P.num_qo_heads % P.num_kv_heads != 0) {
+        err = "num_qo_heads must be a positive multiple of num_kv_heads";
+        return MSTAR_ERR_INVALID_ARG;
+    }
+    if (P.head_dim != 64 && P.head_dim != 128) { err = "head_dim must be 64 or 128"; return MSTAR_ERR_UNSUPPORTED; }
+    if (P.page_size != kPage) { err = "page_size must be 16"; return MSTAR_ERR_UNSUPPORTED; }
+    if (P.dtype != MSTAR_DTYPE_F32 && P.dtype != MSTAR_DTYPE_BF16) { err = "dtype must be F32 or BF16"; return MSTAR_ERR_UNSUPPORTED; }
+    if (P.max_blocks_per_seq <= 0 || P.num_pages <= 0) {
+        err = "max_blocks_per_seq and num_pages must be positive";
+        return MSTAR_ERR_INVALID_ARG;
+    }
+    if (!std::isfinite(P.sm_scale)) { err = "sm_scale must be finite"; return MSTAR_ERR_INVALID_ARG; }
+    if ((P.flags & MSTAR_FLAG_FORCE_SPLIT) && (P.flags & MSTAR_FLAG_NO_SPLIT)) {
+        err = "FORCE_SPLIT and NO_SPLIT are exclusive";
+        return MSTAR_ERR_INVALID_ARG;
+    }
+    if (P.flags & ~(MSTAR_FLAG_FORCE_SPLIT | MSTAR_FLAG_NO_SPLIT)) { err = "unknown flag"; return MSTAR_ERR_INVALID_ARG; }
+
+    plan = HostPlan();
+    plan.params = P;
+    plan.num_seqs = num_seqs;
+    const int32_t G = P.num_qo_heads / P.num_kv_heads;
+    plan.group = G;
+    const int64_t max_kv = (int64_t)P.max_blocks_per_seq * kPage;
+
+    // ---- 1. validate requests, 2. row intervals --------------------------
+    std::vector<std::pair<int64_t, int64_t>> ranges;
+    std::vector<RowIntervals> iv(num_seqs);
+    int64_t total_q = 0;
+    for (int32_t r = 0; r < num_seqs; ++r) {
+        const mstar_seq_desc& s = seqs[r];
+        const mstar_mask_spec& m = masks[r];
+        char buf[160];
+        if (s.q_len < 0 || s.kv_len < s.q_len || s.q_start < 0) {
+            snprintf(buf, sizeof buf, "request %d: need 0 <= q_len <= kv_len and q_start >= 0", r);
+            err = buf;
+            return MSTAR_ERR_INVALID_ARG;
+        }
+        if (s.kv_len > max_kv) {
+            snprintf(buf, sizeof buf, "request %d: kv_len exceeds 16 * max_blocks_per_seq", r);
+            err = buf;
+            return MSTAR_ERR_INVALID_ARG;
+        }
+        if (m.window < 0 || m.seg_begin < 0 || m.seg_count < 0 || (int64_t)m.seg_begin + m.seg_count > num_segs) {
+            snprintf(buf, sizeof buf, "request %d: bad mask spec (window < 0 or segment range)", r);
+            err = buf;
+            return MSTAR_ERR_INVALID_ARG;
+        }
+        if ((int64_t)s.q_start + s.q_len > INT32_MAX / P.num_qo_heads) {
+            snprintf(buf, sizeof buf, "request %d: too many query rows", r);
+            err = buf;
+            return MSTAR_ERR_INVALID_ARG;
+        }
+        std::string e2;
+        if (!row_intervals(s, m, segs, iv[r], e2)) {
+            snprintf(buf, sizeof buf, "request %d: ", r);
+            err = buf + e2;
+            return MSTAR_ERR_INVALID_ARG;
+        }
+        if (s.q_len > 0) ranges.push_back({s.q_start, (int64_t)s.q_start + s.q_len});
+        total_q = std::max<int64_t>(total_q, (int64_t)s.q_start + s.q_len);
+    }
+    std::sort(ranges.begin(), ranges.end());
+    for (size_t i = 1; i < ranges.size(); ++i) {
+        if (ranges[i].first < ranges[i - 1].second) {
+            err = "query row ranges of two requests overlap";
+            return MSTAR_ERR_INVALID_ARG;
+        }
+    }
+    plan.total_q = (int32_t)total_q;
+
+    plan.seqs.resize(num_seqs);
+    plan.key_lo.assign(num_seqs, 0);
+    plan.key_hi.assign(num_seqs, 0);
+    for (int32_t r = 0; r < num_seqs; ++r) {
+        const mstar_seq_desc& s = seqs[r];
+        SeqInfo& si = plan.seqs[r];
+        si.q_len = s.q_len;
+        si.kv_len = s.kv_len;
+        si.q_start = s.q_start;
+        si.window = masks[r].window;
+        si.hi_off = (int32_t)plan.row_hi.size();
+        si.seq_index = r;
+        si.pad0 = si.pad1 = 0;
+        plan.row_hi.insert(plan.row_hi.end(), iv[r].hi.begin(), iv[r].hi.end());
+        for (int32_t i = 0; i < s.q_len; ++i) plan.visible_pairs += (int64_t)(iv[r].hi[i] - iv[r].lo[i]);
+        if (s.q_len > 0) {
+            plan.key_lo[r] = iv[r].lo[0];
+            plan.key_hi[r] = iv[r].hi[s.q_len - 1];
+        }
+    }
+    plan.visible_pairs *= P.num_qo_heads;
+    while (plan.row_hi.size() % 8) plan.row_hi.push_back(0);
+
+    // ---- 3. work units ----------------------------------------------------
+    std::vector<Unit> few_units, tile_units;
+    for (int32_t r = 0; r < num_seqs; ++r) {
+        const mstar_seq_desc& s = seqs[r];
+        if (s.q_len == 0) continue;
+        const RowIntervals& v = iv[r];
+        if (P.dtype == MSTAR_DTYPE_F32) {
+            for (int32_t h = 0; h < P.num_qo_heads; ++h) {
+                for (int32_t row0 = 0; row0 < s.q_len; row0 += kF32Rows) {
+                    const int32_t nr = std::min(kF32Rows, s.q_len - row0);
+                    WorkItem w{r, h, row0, nr, align_down16(v.lo[row0]), v.hi[row0 + nr - 1], -1, 0};
+                    plan.f32.push_back(w);
+                }
+            }
+            continue;
+        }
+        const int64_t R = (int64_t)s.q_len * G;
+        if (R <= kDecodeMaxRows) {
+            for (int32_t kvh = 0; kvh < P.num_kv_heads; ++kvh) {
+                Unit u{r, kvh, 0, (int32_t)R, align_down16(v.lo[0]), v.hi[s.q_len - 1], 0};
+                u.cost = (int64_t)(u.k_end - u.k_begin);
+                few_units.push_back(u);
+            }
+            plan.decode_rb = std::max<int32_t>(plan.decode_rb, R <= 16 ? 1 : R <= 32 ? 2 : 4);
+        } else {
+            for (int32_t h = 0; h < P.num_qo_heads; ++h) {
+                for (int32_t row0 = 0; row0 < s.q_len; row0 += kTileRows) {
+                    const int32_t nr = std::min(kTileRows, s.q_len - row0);
+                    Unit u{r, h, row0, nr, align_down16(v.lo[row0]), v.hi[row0 + nr - 1], 0};
+                    tile_units.push_back(u);
+                }
+            }
+        }
+    }
+
+    // ---- 4. key splitting ---------------------------------------------------
+    int64_t slot = 0;
+    auto emit = [&](const Unit& u, int32_t chunk, int32_t align, std::vector<WorkItem>& dst, bool few) {
+        const int64_t n = (int64_t)u.k_end - u.k_begin;
+        int64_t nch = 1, cs = n;
+        if (chunk > 0 && n > chunk) {
+            nch = ceil_div(n, chunk);
+            cs = ceil_div(ceil_div(n, nch), align) * align;
+            nch = ceil_div(n, cs);
+        }
+        const int32_t G_ = few ? G : 1;
+        for (int64_t c = 0; c < nch; ++c) {
+            WorkItem w;
+            w.seq = u.seq;
+            w.head = u.head;
+            w.row0 = u.row0;
+            w.nrows = u.nrows;
+            w.k_begin = (int32_t)(u.k_begin + c * cs);
+            w.k_end = (int32_t)std::min<int64_t>(u.k_begin + (c + 1) * cs, u.k_end);
+            w.part = nch > 1 ? (int32_t)(slot + c * u.nrows) : -1;
+            w.pad = 0;
+            dst.push_back(w);
+        }
+        if (nch > 1) {
+            const SeqInfo& si = plan.seqs[u.seq];
+            for (int32_t r = 0; r < u.nrows; ++r) {
+                MergeItem m;
+                const int32_t rr = u.row0 + r;
+                m.row = si.q_start + rr / G_;
+                m.head = few ? u.head * G + rr % G : u.head;
+                m.slot0 = (int32_t)(slot + r);
+                m.stride = u.nrows;
+                m.nslots = (int32_t)nch;
+                m.pad0 = m.pad1 = m.pad2 = 0;
+                plan.merges.push_back(m);
+            }
+            slot += nch * u.nrows;
+        }
+    };
+
+    {  // few-row units: enough items to keep every CU streaming K/V
+        int64_t total = 0;
+        for (const Unit& u : few_units) total += u.k_end - u.k_begin;
+        int32_t chunk = 0;
+        if (P.flags & MSTAR_FLAG_FORCE_SPLIT) {
+            chunk = kSubKeys * 2;
+        } else if (!(P.flags & MSTAR_FLAG_NO_SPLIT)) {
+            const int64_t target_items = 2048;
+            int64_t c = std::max<int64_t>(256, ceil_div(total, target_items));
+            chunk = (int32_t)std::min<int64_t>(ceil_div(c, 128) * 128, INT32_MAX / 2);
+        }
+        for (const Unit& u : few_units) emit(u, chunk, kSubKeys, plan.few, true);
+    }
+    {  // multi-row tiles: split only when the tiles alone cannot fill the GPU
+        int64_t total = 0;
+        for (const Unit& u : tile_units) total += u.k_end - u.k_begin;
+        int32_t chunk = 0;
+        if (P.flags & MSTAR_FLAG_FORCE_SPLIT) {
+            chunk = kTileKeys * 2;
+        } else if (!(P.flags & MSTAR_FLAG_NO_SPLIT) && tile_units.size() < 512 && !tile_units.empty()) {
+            int64_t c = std::max<int64_t>(1024, ceil_div(total, 1024));
+            chunk = (int32_t)std::min<int64_t>(ceil_div(c, kTileKeys) * kTileKeys, INT32_MAX / 2);
+        }
+        for (const Unit& u : tile_units) emit(u, chunk, kTileKeys, plan.tiles, false);
+    }
+    plan.partial_slots = slot;
+    if (slot > INT32_MAX) { err = "too many partial rows"; return MSTAR_ERR_INVALID_ARG; }
+
+    // ---- 5. longest first ------------------------------------------------------
+    auto visible_in = [&](const WorkItem& w) -> int64_t {
+        const RowIntervals& v = iv[w.seq];
+        int64_t c = 0;
+        for (int32_t r = 0; r < w.nrows; ++r) {
+            const int32_t i = w.row0 + r;
+            const int32_t a = std::max(v.lo[i], w.k_begin), b = std::min(v.hi[i], w.k_end);
+            if (b > a) c += b - a;
+        }
+        return c;
+    };
+    auto lpt = [&](std::vector<WorkItem>& items, bool by_pairs) {
+        std::vector<std::pair<int64_t, int32_t>> key(items.size());
+        for (size_t i = 0; i < items.size(); ++i)
+            key[i] = {by_pairs ? visible_in(items[i]) : (int64_t)(items[i].k_end - items[i].k_begin), (int32_t)i};
+        std::stable_sort(key.begin(), key.end(), [](const auto& a, const auto& b) { return a.first > b.first; });
+        std::vector<WorkItem> sorted(items.size());
+        for (size_t i = 0; i < items.size(); ++i) sorted[i] = items[key[i].second];
+        items.swap(sorted);
+    };
+    lpt(plan.tiles, true);
+    lpt(plan.few, false);
+    lpt(plan.f32, true);
+    return MSTAR_OK;
+}
+
+}  // namespace mstar

@@ -1,0 +1,37 @@
+// Host planner: mask descriptors -> per-row visible intervals -> work items.
+// Pure C++ (no HIP); the C-ABI layer uploads what it produces.
+#pragma once
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/mstar_attn.h"
+#include "plan_types.h"
+
+namespace mstar {
+
+struct HostPlan {
+    mstar_attn_params params{};
+    int32_t num_seqs = 0;
+    int32_t total_q = 0;
+    int32_t group = 1;       // Hq / Hkv
+    int32_t decode_rb = 1;   // 16-row blocks per few-row item (1, 2 or 4)
+    std::vector<SeqInfo> seqs;
+    std::vector<int32_t> row_hi;
+    std::vector<int32_t> key_lo, key_hi;  // per request union of visible keys
+    std::vector<WorkItem> tiles;          // multi-row kernel
+    std::vector<WorkItem> few;            // few-row kernel
+    std::vector<WorkItem> f32;            // fp32 kernel
+    std::vector<MergeItem> merges;
+    int64_t visible_pairs = 0;
+    int64_t partial_slots = 0;
+};
+
+// Fills `plan` from the descriptors.  Returns MSTAR_OK or an MSTAR_ERR_* code
+// with a message in `err`.
+int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
+                    const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segs,
+                    int32_t num_segs, HostPlan& plan, std::string& err);
+
+}  // namespace mstar

@@ -1,0 +1,194 @@
+"""GPU parity: the HIP path through the C-ABI against the CPU fp64 oracle.
+
+Tolerances (max-abs over every compared element, unit-variance inputs):
+out 1e-5 (fp32) / 1.5e-2 (bf16), lse 1e-3 (natural log)."""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import oracle_attention, oracle_rows
+from paper_2606_12688_amd import attn
+from tests.helpers import plan_for, run_gpu
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+TOL = {"f32": (1e-5, 1e-3), "bf16": (1.5e-2, 1e-3)}
+
+
+def _host(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def _compare(b, out, lse, ref_o, ref_l, label=""):
+    tol_o, tol_l = TOL[b.dtype]
+    o = _host(out)
+    l = lse.cpu().numpy().astype(np.float64)
+    assert np.isfinite(o).all(), f"{label}: non-finite output"
+    assert np.isfinite(l).all(), f"{label}: non-finite lse"
+    eo = float(np.abs(o - ref_o).max()) if o.size else 0.0
+    el = float(np.abs(l - ref_l).max()) if l.size else 0.0
+    print(f"{label}: max|dout|={eo:.3e} max|dlse|={el:.3e}", flush=True)
+    assert eo <= tol_o, f"{label}: out error {eo} > {tol_o}"
+    assert el <= tol_l, f"{label}: lse error {el} > {tol_l}"
+
+
+def _oracle(b, t):
+    h = {k: _host(v) for k, v in t.items()}
+    return oracle_attention(b, h["q"], h["k_pages"], h["v_pages"])
+
+
+REDUCED = ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16", "rollout_bf16", "mixed"]
+FLAGS = {"auto": 0, "force_split": attn.FLAG_FORCE_SPLIT, "no_split": attn.FLAG_NO_SPLIT}
+
+
+@pytest.mark.parametrize("flag", list(FLAGS))
+@pytest.mark.parametrize("name", REDUCED)
+def test_reduced_parity(name, flag):
+    b = W.reduced(name)
+    t = W.make_tensors_torch(b, DEV)
+    out, lse = run_gpu(b, t, FLAGS[flag])
+    ro, rl = _oracle(b, t)
+    _compare(b, out, lse, ro, rl, f"{name}/{flag}")
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+@pytest.mark.parametrize("name", ["tiny_causal_f32", "decode_bf16"])
+def test_more_seeds(name, seed):
+    b = W.reduced(name, seed)
+    t = W.make_tensors_torch(b, DEV)
+    out, lse = run_gpu(b, t)
+    _compare(b, out, lse, *_oracle(b, t), f"{name}/seed{seed}")
+
+
+@pytest.mark.parametrize("d,hq,hkv,dtype", [(64, 8, 2, "bf16"), (64, 4, 4, "bf16"), (128, 6, 6, "bf16"),
+                                            (128, 12, 2, "bf16"), (64, 4, 2, "f32"), (128, 2, 1, "f32")])
+def test_mixed_launch_head_layouts(d, hq, hkv, dtype):
+    b = W.mixed(seed=3, hq=hq, hkv=hkv, d=d, dtype=dtype)
+    t = W.make_tensors_torch(b, DEV)
+    for flag in (0, attn.FLAG_FORCE_SPLIT):
+        out, lse = run_gpu(b, t, flag)
+        _compare(b, out, lse, *_oracle(b, t), f"mixed d{d} {hq}/{hkv} {dtype} flags{flag}")
+
+
+def test_determinism_and_page_permutation_bitwise():
+    import torch
+
+    b = W.reduced("mixed")
+    t = W.make_tensors_torch(b, DEV)
+    o1, l1 = run_gpu(b, t)
+    o2, l2 = run_gpu(b, t)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1.view(torch.int32), l2.view(torch.int32))
+    b2, t2 = W.permute_pages(b, t, seed=11)
+    o3, l3 = run_gpu(b2, t2)
+    assert torch.equal(o1.view(torch.int16), o3.view(torch.int16))
+    assert torch.equal(l1.view(torch.int32), l3.view(torch.int32))
+
+
+def test_unused_slots_poisoned_with_nan():
+    for name in ("mixed", "decode_bf16", "rollout_bf16", "tiny_causal_f32"):
+        b = W.reduced(name)
+        t = W.make_tensors_torch(b, DEV, poison_unused=True)
+        for flag in (0, attn.FLAG_FORCE_SPLIT):
+            out, lse = run_gpu(b, t, flag)
+            _compare(b, out, lse, *_oracle(b, t), f"{name} NaN-poisoned flags{flag}")
+
+
+def test_out_of_range_page_sets_error_bit_without_reading():
+    import torch
+
+    b = W.reduced("decode_bf16")
+    t = W.make_tensors_torch(b, DEV)
+    bt = b.block_table.copy()
+    bt[0, 0] = b.num_pages + 5
+    bt[1, 0] = -3
+    pl = plan_for(b)
+    out = torch.zeros_like(t["q"])
+    lse = torch.zeros(t["q"].shape[:2], dtype=torch.float32, device=DEV)
+    attn.fwd(pl, t["q"], t["k_pages"], t["v_pages"], torch.from_numpy(bt).to(DEV), out, lse, attn.workspace(pl, DEV))
+    assert attn.check(pl) == attn.DEVERR_PAGE_RANGE
+    assert attn.check(pl) == 0  # the word was cleared
+    assert torch.isfinite(out.float()).all()
+    pl.destroy()
+
+
+def test_fwd_rejects_wrong_shapes_and_small_workspace():
+    import torch
+
+    b = W.reduced("decode_bf16")
+    t = W.make_tensors_torch(b, DEV)
+    pl = plan_for(b, attn.FLAG_FORCE_SPLIT)
+    bt = torch.from_numpy(b.block_table).to(DEV)
+    out = torch.empty_like(t["q"])
+    lse = torch.empty(t["q"].shape[:2], dtype=torch.float32, device=DEV)
+    with pytest.raises(ValueError):
+        attn.fwd(pl, t["q"][:-1], t["k_pages"], t["v_pages"], bt, out, lse, attn.workspace(pl, DEV))
+    with pytest.raises(attn.MStarError) as ei:
+        attn.fwd(pl, t["q"], t["k_pages"], t["v_pages"], bt, out, lse, None)
+    assert ei.value.code == attn.ERR_WORKSPACE
+    small = torch.empty(16, dtype=torch.uint8, device=DEV)
+    rc = attn.lib().mstar_attn_fwd(pl.handle, t["q"].data_ptr(), t["k_pages"].data_ptr(), t["v_pages"].data_ptr(),
+                                   bt.data_ptr(), out.data_ptr(), lse.data_ptr(), small.data_ptr(), 16, None)
+    assert rc == attn.ERR_WORKSPACE
+    pl.destroy()
+
+
+# ---------------------------------------------------------------------------
+# Full sizes: sampled outputs against the oracle, and a property of every row.
+# ---------------------------------------------------------------------------
+
+def _sub_batch(b, t, reqs):
+    """The requests `reqs` as a batch of their own (their pages copied to the
+    host), for the oracle."""
+    import torch
+
+    reqs = list(reqs)
+    bt = b.block_table[reqs]
+    pages = np.unique(bt[bt >= 0])
+    idx = torch.from_numpy(pages.astype(np.int64)).to(DEV)
+    kp = _host(t["k_pages"].index_select(0, idx))
+    vp = _host(t["v_pages"].index_select(0, idx))
+    nbt = np.where(bt >= 0, np.searchsorted(pages, bt), -1).astype(np.int32)
+    seqs = b.seqs[reqs].copy()
+    rows = np.concatenate([np.arange(s[2], s[2] + s[0]) for s in b.seqs[reqs]])
+    qs = np.concatenate([[0], np.cumsum(seqs[:-1, 0])])
+    seqs[:, 2] = qs
+    segl = [[tuple(x) for x in b.seq_segments(r)] for r in reqs]
+    sb = W._finish("sub", b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, list(seqs[:, 0]),
+                   list(seqs[:, 1]), segl, list(b.masks[reqs, 2]), nbt, len(pages), 0)
+    q = _host(t["q"].index_select(0, torch.from_numpy(rows).to(DEV)))
+    return sb, q, kp, vp, rows
+
+
+@pytest.mark.parametrize("name", ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16",
+                                  "rollout_bf16"])
+def test_full_size_sampled(name):
+    import torch
+
+    b = W.FULL_SIZE[name]()
+    print(f"{name}: generating", flush=True)
+    t = W.make_tensors_torch(b, DEV)
+    out, lse = run_gpu(b, t)
+    torch.cuda.synchronize()
+    print(f"{name}: fwd done", flush=True)
+    # every output is a convex combination of value rows
+    vmax = float(t["v_pages"].float().abs().max())
+    assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all()
+    assert float(out.float().abs().max()) <= vmax * (1 + 2 ** -7)
+    rng = np.random.default_rng(7)
+    n = b.num_seqs
+    reqs = sorted({0, n - 1, *rng.choice(n, size=min(n, 4), replace=False).tolist()})
+    sb, q, kp, vp, rows = _sub_batch(b, t, reqs)
+    picks = []
+    for j in range(sb.num_seqs):
+        ql = int(sb.seqs[j, 0])
+        for i in sorted({0, ql - 1, *rng.integers(0, ql, size=3).tolist()}):
+            for h in sorted({0, b.num_qo_heads - 1, int(rng.integers(b.num_qo_heads))}):
+                picks.append((j, i, h))
+    ro, rl = oracle_rows(sb, q, kp, vp, picks)
+    got_o = np.stack([_host(out[rows[sb.seqs[j, 2] + i], h]) for j, i, h in picks])
+    got_l = np.array([float(lse[rows[sb.seqs[j, 2] + i], h]) for j, i, h in picks])
+    tol_o, tol_l = TOL[b.dtype]
+    eo, el = float(np.abs(got_o - ro).max()), float(np.abs(got_l - rl).max())
+    print(f"{name} full size, {len(picks)} sampled rows: max|dout|={eo:.3e} max|dlse|={el:.3e}", flush=True)
+    assert eo <= tol_o and el <= tol_l
