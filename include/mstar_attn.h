@@ -159,7 +159,9 @@ size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan);
  * overwrites it.  Enqueues at most four kernels; no allocation, no host
  * synchronization and no host reads, so the call may be captured in a HIP
  * graph.  The same plan may run with any tensors of the planned shapes.  Two
- * fwd calls that overlap in time must use different workspaces.  Block-table
+ * fwd calls that overlap in time must use different plans and different
+ * workspaces (the plan holds the split-K arrival counters, which every call
+ * returns to zero).  Block-table
  * entries outside [0, num_pages) are never dereferenced: they read as zeros
  * and set MSTAR_DEVERR_PAGE_RANGE in the plan's device error word.
  * Errors: INVALID_ARG (null tensor pointer, misaligned pointer), WORKSPACE,
@@ -180,13 +182,16 @@ int mstar_attn_plan_stats(const mstar_plan_t* plan, mstar_plan_stats* out);
  * (0, 0 for a request without queries). */
 int mstar_attn_plan_key_ranges(const mstar_plan_t* plan, int32_t* lo_hi, int32_t num_seqs);
 
-/* Copy the host-side work list of one kernel class (0 = multi-row tiles,
- * 1 = few-row items, 2 = fp32 items, 3 = merge rows) into `items` as int32
+/* Copy one host-side list of the plan (0 = multi-row tiles, 1 = few-row
+ * items, 2 = fp32 items, 3 = rows merged by the merge kernel, 4 = split
+ * few-row units, merged inside the few-row kernel) into `items` as int32
  * records of 8 fields; *count receives the number of records, and at most
  * `capacity` records are written.  For inspection and tests.
  * Work record: seq, head (query head; KV head for class 1), row0, nrows,
- *              key_begin, key_end, partial_slot (-1 = final), 0.
- * Merge record: packed_row, head, slot0, slot_stride, nslots, 0, 0, 0. */
+ *              key_begin, key_end, partial_slot (-1 = final), split unit (-1 = none).
+ * Merge record: packed_row, head, slot0, slot_stride, nslots, 0, 0, 0.
+ * Unit record: slot0, nchunks, rows, seq, kv_head, row0, 0, 0 (chunk c, row r
+ *              -> partial slot slot0 + c * rows + r). */
 int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, int32_t* items,
                           int64_t capacity, int64_t* count);
 

@@ -20,7 +20,8 @@ struct mstar_plan {
     void* dev = nullptr;     // device copy of the plan blob
     void* pinned = nullptr;  // pinned staging copy (kept until destroy)
     size_t bytes = 0;
-    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_err = 0;
+    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_units = 0,
+           off_counters = 0, off_err = 0;
     double plan_us = 0.0;
 };
 
@@ -80,7 +81,7 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     }
     const mstar::HostPlan& h = plan->host;
 
-    // blob layout: seqs | row_hi | tiles | few | f32 | merges | error word
+    // blob layout: seqs | row_hi | tiles | few | f32 | merges | units | counters | error word
     size_t off = 0;
     plan->off_seqs = off;   off = align256(off + h.seqs.size() * sizeof(mstar::SeqInfo));
     plan->off_row_hi = off; off = align256(off + h.row_hi.size() * sizeof(int32_t));
@@ -88,6 +89,8 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     plan->off_few = off;    off = align256(off + h.few.size() * sizeof(mstar::WorkItem));
     plan->off_f32 = off;    off = align256(off + h.f32.size() * sizeof(mstar::WorkItem));
     plan->off_merge = off;  off = align256(off + h.merges.size() * sizeof(mstar::MergeItem));
+    plan->off_units = off;  off = align256(off + h.units.size() * sizeof(mstar::SplitUnit));
+    plan->off_counters = off; off = align256(off + h.units.size() * sizeof(int32_t));
     plan->off_err = off;    off = align256(off + sizeof(int32_t));
     plan->bytes = off;
 
@@ -105,6 +108,7 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
         put(blob, plan->off_few, h.few);
         put(blob, plan->off_f32, h.f32);
         put(blob, plan->off_merge, h.merges);
+        put(blob, plan->off_units, h.units);  // counters and error word stay zero
         e = hipMalloc(&plan->dev, plan->bytes);
         if (e != hipSuccess) {
             (void)hipHostFree(plan->pinned);
@@ -164,6 +168,8 @@ MSTAR_EXPORT int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const v
                                                      align256((size_t)h.partial_slots * D * sizeof(float)))
                           : nullptr;
     a.err = reinterpret_cast<int32_t*>(blob + plan->off_err);
+    a.units = reinterpret_cast<const mstar::SplitUnit*>(blob + plan->off_units);
+    a.counters = reinterpret_cast<int32_t*>(blob + plan->off_counters);
     a.hq = h.params.num_qo_heads;
     a.hkv = h.params.num_kv_heads;
     a.group = h.group;
@@ -232,7 +238,7 @@ MSTAR_EXPORT int mstar_attn_plan_stats(const mstar_plan_t* plan, mstar_plan_stat
     out->prefill_items = (int64_t)h.tiles.size();
     out->decode_items = (int64_t)h.few.size();
     out->f32_items = (int64_t)h.f32.size();
-    out->merge_rows = (int64_t)h.merges.size();
+    out->merge_rows = h.merged_rows;
     out->partial_slots = h.partial_slots;
     out->total_q = h.total_q;
     out->plan_host_us = plan->plan_us;
@@ -260,7 +266,8 @@ MSTAR_EXPORT int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, i
         case 1: src = h.few.data(); n = h.few.size(); break;
         case 2: src = h.f32.data(); n = h.f32.size(); break;
         case 3: src = h.merges.data(); n = h.merges.size(); break;
-        default: return fail(MSTAR_ERR_INVALID_ARG, "kind must be 0..3");
+        case 4: src = h.units.data(); n = h.units.size(); break;
+        default: return fail(MSTAR_ERR_INVALID_ARG, "kind must be 0..4");
     }
     *count = (int64_t)n;
     if (capacity > 0 && !items) return fail(MSTAR_ERR_INVALID_ARG, "items is NULL");

@@ -511,6 +511,43 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
             if (d4 == 0) a.part_lse[slot] = lse;
         }
     }
+    if (it.unit < 0) return;
+
+    // ---- split unit: the last chunk to finish merges the unit's partials ------
+    __shared__ int is_last;
+    __threadfence();  // release: this chunk's partials are visible device-wide
+    __syncthreads();
+    if (tid == 0) {
+        const int prev = atomicAdd(&a.counters[it.unit], 1);
+        is_last = prev == a.units[it.unit].nch - 1;
+    }
+    __syncthreads();
+    if (!is_last) return;
+    __threadfence();  // acquire: see every other chunk's partials
+    const SplitUnit u = a.units[it.unit];
+    for (int e = tid; e < NV; e += 256) {
+        const int row = e / (D / 4), d4 = (e % (D / 4)) * 4;
+        if (row >= u.rows) continue;
+        float mstar = kNegInf;
+        for (int c = 0; c < u.nch; ++c) mstar = fmaxf(mstar, a.part_lse[u.slot0 + (int64_t)c * u.rows + row]);
+        f32x4 acc = {0, 0, 0, 0};
+        float tot = 0.0f;
+        if (mstar != kNegInf) {
+            for (int c = 0; c < u.nch; ++c) {
+                const int64_t slot = u.slot0 + (int64_t)c * u.rows + row;
+                const float w = expf(a.part_lse[slot] - mstar);
+                tot += w;
+                acc += w * *reinterpret_cast<const f32x4*>(a.part_o + slot * D + d4);
+            }
+        }
+        const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
+        const int rr = u.row0 + row;
+        const int64_t orow = (int64_t)(si.q_start + rr / G) * a.hq + u.head * G + rr % G;
+        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16_t*>(a.out) + orow * D + d4) =
+            __builtin_convertvector(acc * inv, bf16x4);
+        if (d4 == 0) a.lse[orow] = tot > 0.0f ? mstar + logf(tot) : kNegInf;
+    }
+    if (tid == 0) atomicExch(&a.counters[it.unit], 0);  // ready for the next call
 }
 
 // ---------------------------------------------------------------------------

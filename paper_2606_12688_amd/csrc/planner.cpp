@@ -255,10 +255,22 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             w.k_begin = (int32_t)(u.k_begin + c * cs);
             w.k_end = (int32_t)std::min<int64_t>(u.k_begin + (c + 1) * cs, u.k_end);
             w.part = nch > 1 ? (int32_t)(slot + c * u.nrows) : -1;
-            w.pad = 0;
+            w.unit = (nch > 1 && few) ? (int32_t)plan.units.size() : -1;
             dst.push_back(w);
         }
-        if (nch > 1) {
+        if (nch > 1) plan.merged_rows += u.nrows;
+        if (nch > 1 && few) {
+            SplitUnit su;
+            su.slot0 = (int32_t)slot;
+            su.nch = (int32_t)nch;
+            su.rows = u.nrows;
+            su.seq = u.seq;
+            su.head = u.head;
+            su.row0 = u.row0;
+            su.pad0 = su.pad1 = 0;
+            plan.units.push_back(su);
+            slot += nch * u.nrows;
+        } else if (nch > 1) {
             const SeqInfo& si = plan.seqs[u.seq];
             for (int32_t r = 0; r < u.nrows; ++r) {
                 MergeItem m;

@@ -137,29 +137,6 @@ def test_fwd_rejects_wrong_shapes_and_small_workspace():
 # Full sizes: sampled outputs against the oracle, and a property of every row.
 # ---------------------------------------------------------------------------
 
-def _sub_batch(b, t, reqs):
-    """The requests `reqs` as a batch of their own (their pages copied to the
-    host), for the oracle."""
-    import torch
-
-    reqs = list(reqs)
-    bt = b.block_table[reqs]
-    pages = np.unique(bt[bt >= 0])
-    idx = torch.from_numpy(pages.astype(np.int64)).to(DEV)
-    kp = _host(t["k_pages"].index_select(0, idx))
-    vp = _host(t["v_pages"].index_select(0, idx))
-    nbt = np.where(bt >= 0, np.searchsorted(pages, bt), -1).astype(np.int32)
-    seqs = b.seqs[reqs].copy()
-    rows = np.concatenate([np.arange(s[2], s[2] + s[0]) for s in b.seqs[reqs]])
-    qs = np.concatenate([[0], np.cumsum(seqs[:-1, 0])])
-    seqs[:, 2] = qs
-    segl = [[tuple(x) for x in b.seq_segments(r)] for r in reqs]
-    sb = W._finish("sub", b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, list(seqs[:, 0]),
-                   list(seqs[:, 1]), segl, list(b.masks[reqs, 2]), nbt, len(pages), 0)
-    q = _host(t["q"].index_select(0, torch.from_numpy(rows).to(DEV)))
-    return sb, q, kp, vp, rows
-
-
 @pytest.mark.parametrize("name", ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16",
                                   "rollout_bf16"])
 def test_full_size_sampled(name):
@@ -178,7 +155,7 @@ def test_full_size_sampled(name):
     rng = np.random.default_rng(7)
     n = b.num_seqs
     reqs = sorted({0, n - 1, *rng.choice(n, size=min(n, 4), replace=False).tolist()})
-    sb, q, kp, vp, rows = _sub_batch(b, t, reqs)
+    sb, q, kp, vp, rows = W.extract_requests(b, t, reqs, _host)
     picks = []
     for j in range(sb.num_seqs):
         ql = int(sb.seqs[j, 0])

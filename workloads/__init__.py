@@ -369,3 +369,33 @@ def _as_index(x, idx):
     import torch
 
     return torch.from_numpy(idx.astype(np.int64)).to(x.device)
+
+
+def extract_requests(b: Batch, tensors: dict, reqs, to_host=None):
+    """The requests ``reqs`` of ``b`` as a batch of their own, with only their
+    pages (renumbered) and their query rows.  ``tensors`` may live on any
+    device; ``to_host`` converts a tensor to a float64 numpy array (default:
+    ``.float().cpu().numpy()``).  Returns ``(sub_batch, q, k_pages, v_pages,
+    rows)`` where ``rows`` are the packed query rows of the originals."""
+    reqs = [int(r) for r in reqs]
+    if to_host is None:
+        def to_host(t):
+            return np.asarray(t.float().cpu().numpy(), dtype=np.float64) if not isinstance(t, np.ndarray) \
+                else np.asarray(t, dtype=np.float64)
+    bt = b.block_table[reqs]
+    pages = np.unique(bt[bt >= 0])
+    nbt = np.where(bt >= 0, np.searchsorted(pages, bt), -1).astype(np.int32)
+    seqs = b.seqs[reqs].copy()
+    rows = np.concatenate([np.arange(s[2], s[2] + s[0]) for s in b.seqs[reqs]]).astype(np.int64)
+    segl = [[tuple(int(v) for v in x) for x in b.seq_segments(r)] for r in reqs]
+    sb = _finish(b.name + "/sub", b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, [int(x) for x in seqs[:, 0]],
+                 [int(x) for x in seqs[:, 1]], segl, [int(x) for x in b.masks[reqs, 2]], nbt, len(pages), b.seed)
+    kp, vp, q = tensors["k_pages"], tensors["v_pages"], tensors["q"]
+    if isinstance(kp, np.ndarray):
+        return sb, to_host(q[rows]), to_host(kp[pages]), to_host(vp[pages]), rows
+    import torch
+
+    pidx = torch.from_numpy(pages.astype(np.int64)).to(kp.device)
+    ridx = torch.from_numpy(rows).to(q.device)
+    return sb, to_host(q.index_select(0, ridx)), to_host(kp.index_select(0, pidx)), \
+        to_host(vp.index_select(0, pidx)), rows
