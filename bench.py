@@ -23,6 +23,7 @@ K and once for V, pages shared between requests once.
 from __future__ import annotations
 
 import argparse
+import ctypes
 import hashlib
 import json
 import os
@@ -40,6 +41,10 @@ PEAK_BF16_TFLOPS = 2516.6   # dense MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
 PEAK_FP32_TFLOPS = 157.3
 BOUND = {"tiny_causal_f32": "alu", "decode_bf16": "hbm", "text_latent_bf16": "mfma",
          "stream_window_bf16": "hbm", "rollout_bf16": "mfma"}
+# kernel classes of mstar_attn_fwd_timed: 0 multi-row tiles, 1 few-row items, 2 fp32, 3 merge
+KERNEL_NAMES = ["tile_kernel", "few_kernel", "f32_kernel", "merge_kernel"]
+DOMINANT = {"tiny_causal_f32": 2, "decode_bf16": 1, "text_latent_bf16": 0, "stream_window_bf16": 1,
+            "rollout_bf16": 0}
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_12688_amd", "csrc", "kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -172,26 +177,40 @@ def main():
     calls = [(pl.handle, t["q"].data_ptr(), t["k_pages"].data_ptr(), t["v_pages"].data_ptr(), bt.data_ptr(),
               t["out"].data_ptr(), t["lse"].data_ptr(), ws_ptr, ws_n, sh) for t in copies]
 
-    def step(i):
-        rc = L.mstar_attn_fwd(*calls[i % n_rot])
+    # HIP events recorded by the library right before / after each kernel of
+    # every timed step (on the stream the kernels run on)
+    K = args.steps
+    launched = [k for k, n in enumerate(("prefill_items", "decode_items", "f32_items", "merge_rows")) if st[n] > 0]
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(2)] for _ in range(K)]
+    ev_arrays = []
+    for i in range(K):
+        arr = [(ctypes.c_void_p * 4)(), (ctypes.c_void_p * 4)()]
+        for side in range(2):
+            for k in launched:
+                evs[i][side][k].record(stream)  # creates the event
+                arr[side][k] = evs[i][side][k].cuda_event
+        ev_arrays.append(arr)
+
+    def step(i, timed=False):
+        if timed:
+            rc = L.mstar_attn_fwd_timed(*calls[i % n_rot], ev_arrays[i][0], ev_arrays[i][1])
+        else:
+            rc = L.mstar_attn_fwd(*calls[i % n_rot])
         if rc != 0:
             raise attn.MStarError(rc, attn.last_error())
 
     for i in range(args.warmup):
         step(i)
-    K = args.steps
-    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(K):
-        ev0[i].record(stream)
-        step(i)
-        ev1[i].record(stream)
+        step(i, timed=True)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    kernel_ms = np.array([a.elapsed_time(c) for a, c in zip(ev0, ev1)])
     ms_per_step = (t1 - t0) * 1e3 / K
+    per_kernel = {KERNEL_NAMES[k]: np.array([evs[i][0][k].elapsed_time(evs[i][1][k]) for i in range(K)])
+                  for k in launched}
+    kernel_ms = per_kernel[KERNEL_NAMES[DOMINANT[args.workload]]]
     assert attn.check(pl, stream) == 0
 
     tflops = flop / (ms_per_step * 1e-3) / 1e12
@@ -226,8 +245,9 @@ def main():
                      "frac": round(achieved / peak, 4), "traffic": traffic},
         "tflops": round(tflops, 3), "kv_gbps": round(gbps, 3),
         "tflops_frac_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4), "kv_gbps_frac_hbm_peak": round(gbps / PEAK_HBM_GBS, 4),
-        "kernel_ms": {"mean": round(k_mean, 5), "median": round(float(np.median(kernel_ms)), 5),
-                      "p95": round(float(np.percentile(kernel_ms, 95)), 5)},
+        "dominant_kernel": KERNEL_NAMES[DOMINANT[args.workload]],
+        "kernel_ms": {name: {"mean": round(float(v.mean()), 5), "median": round(float(np.median(v)), 5),
+                             "p95": round(float(np.percentile(v, 95)), 5)} for name, v in per_kernel.items()},
         "useful_flop": flop, "kv_bytes": nbytes, "plan_host_us": round(st["plan_host_us"], 1),
         "plan": {k: st[k] for k in ("prefill_items", "decode_items", "f32_items", "merge_rows", "partial_slots")},
         "rotated_input_copies": n_rot, "traffic_note": traffic_note,

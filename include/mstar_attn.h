@@ -156,12 +156,11 @@ size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan);
  * memory, written for every row of every request (rows of no request are
  * untouched).  workspace: caller-owned device memory of at least
  * mstar_attn_workspace_bytes(plan) bytes (may be NULL if that is 0); fwd
- * overwrites it.  Enqueues at most four kernels; no allocation, no host
+ * overwrites it.  Enqueues at most four kernels (multi-row tiles, few-row
+ * items, fp32 items, then the merge of split key ranges); no allocation, no host
  * synchronization and no host reads, so the call may be captured in a HIP
  * graph.  The same plan may run with any tensors of the planned shapes.  Two
- * fwd calls that overlap in time must use different plans and different
- * workspaces (the plan holds the split-K arrival counters, which every call
- * returns to zero).  Block-table
+ * fwd calls that overlap in time must use different workspaces.  Block-table
  * entries outside [0, num_pages) are never dereferenced: they read as zeros
  * and set MSTAR_DEVERR_PAGE_RANGE in the plan's device error word.
  * Errors: INVALID_ARG (null tensor pointer, misaligned pointer), WORKSPACE,
@@ -169,6 +168,17 @@ size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan);
 int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const void* k_pages,
                    const void* v_pages, const int32_t* block_table, void* out, float* lse,
                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* mstar_attn_fwd, additionally recording caller-created HIP events
+ * (hipEvent_t) on `stream` right before and right after each kernel it
+ * enqueues: index 0 = multi-row tile kernel, 1 = few-row kernel, 2 = fp32
+ * kernel, 3 = merge kernel.  Either array, and any entry, may be NULL; events
+ * of kernels the plan does not launch are left untouched.  For per-kernel
+ * timing (profiling); same contract and errors as mstar_attn_fwd. */
+int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, const void* k_pages,
+                         const void* v_pages, const int32_t* block_table, void* out, float* lse,
+                         void* workspace, size_t workspace_bytes, void* stream,
+                         void* const* events_before, void* const* events_after);
 
 /* Synchronize `stream`, then read and clear the plan's sticky device error
  * word into *error_bits (MSTAR_DEVERR_* bits; 0 = no error seen).  Returns
@@ -183,15 +193,12 @@ int mstar_attn_plan_stats(const mstar_plan_t* plan, mstar_plan_stats* out);
 int mstar_attn_plan_key_ranges(const mstar_plan_t* plan, int32_t* lo_hi, int32_t num_seqs);
 
 /* Copy one host-side list of the plan (0 = multi-row tiles, 1 = few-row
- * items, 2 = fp32 items, 3 = rows merged by the merge kernel, 4 = split
- * few-row units, merged inside the few-row kernel) into `items` as int32
- * records of 8 fields; *count receives the number of records, and at most
- * `capacity` records are written.  For inspection and tests.
+ * items, 2 = fp32 items, 3 = rows merged by the merge kernel) into `items` as
+ * int32 records of 8 fields; *count receives the number of records, and at
+ * most `capacity` records are written.  For inspection and tests.
  * Work record: seq, head (query head; KV head for class 1), row0, nrows,
- *              key_begin, key_end, partial_slot (-1 = final), split unit (-1 = none).
- * Merge record: packed_row, head, slot0, slot_stride, nslots, 0, 0, 0.
- * Unit record: slot0, nchunks, rows, seq, kv_head, row0, 0, 0 (chunk c, row r
- *              -> partial slot slot0 + c * rows + r). */
+ *              key_begin, key_end, partial_slot (-1 = final), -1.
+ * Merge record: packed_row, head, slot0, slot_stride, nslots, 0, 0, 0. */
 int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, int32_t* items,
                           int64_t capacity, int64_t* count);
 

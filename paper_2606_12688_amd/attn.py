@@ -36,6 +36,7 @@ EXPORTS = [
     "mstar_attn_plan",
     "mstar_attn_workspace_bytes",
     "mstar_attn_fwd",
+    "mstar_attn_fwd_timed",
     "mstar_attn_check",
     "mstar_attn_plan_stats",
     "mstar_attn_plan_key_ranges",
@@ -97,6 +98,8 @@ def lib() -> ctypes.CDLL:
     L.mstar_attn_workspace_bytes.restype = sz
     L.mstar_attn_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     L.mstar_attn_fwd.restype = ctypes.c_int
+    L.mstar_attn_fwd_timed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp, vp]
+    L.mstar_attn_fwd_timed.restype = ctypes.c_int
     L.mstar_attn_check.argtypes = [vp, vp, ctypes.POINTER(i32)]
     L.mstar_attn_check.restype = ctypes.c_int
     L.mstar_attn_plan_stats.argtypes = [vp, ctypes.POINTER(PlanStats)]

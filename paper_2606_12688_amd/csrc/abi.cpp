@@ -9,7 +9,7 @@
 #include <new>
 #include <string>
 
-#include "../../include/mstar_attn.h"
+#include "mstar_attn.h"
 #include "kernels.h"
 #include "planner.h"
 
@@ -20,8 +20,7 @@ struct mstar_plan {
     void* dev = nullptr;     // device copy of the plan blob
     void* pinned = nullptr;  // pinned staging copy (kept until destroy)
     size_t bytes = 0;
-    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_units = 0,
-           off_counters = 0, off_err = 0;
+    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_err = 0;
     double plan_us = 0.0;
 };
 
@@ -81,7 +80,7 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     }
     const mstar::HostPlan& h = plan->host;
 
-    // blob layout: seqs | row_hi | tiles | few | f32 | merges | units | counters | error word
+    // blob layout: seqs | row_hi | tiles | few | f32 | merges | error word
     size_t off = 0;
     plan->off_seqs = off;   off = align256(off + h.seqs.size() * sizeof(mstar::SeqInfo));
     plan->off_row_hi = off; off = align256(off + h.row_hi.size() * sizeof(int32_t));
@@ -89,8 +88,6 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     plan->off_few = off;    off = align256(off + h.few.size() * sizeof(mstar::WorkItem));
     plan->off_f32 = off;    off = align256(off + h.f32.size() * sizeof(mstar::WorkItem));
     plan->off_merge = off;  off = align256(off + h.merges.size() * sizeof(mstar::MergeItem));
-    plan->off_units = off;  off = align256(off + h.units.size() * sizeof(mstar::SplitUnit));
-    plan->off_counters = off; off = align256(off + h.units.size() * sizeof(int32_t));
     plan->off_err = off;    off = align256(off + sizeof(int32_t));
     plan->bytes = off;
 
@@ -108,7 +105,6 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
         put(blob, plan->off_few, h.few);
         put(blob, plan->off_f32, h.f32);
         put(blob, plan->off_merge, h.merges);
-        put(blob, plan->off_units, h.units);  // counters and error word stay zero
         e = hipMalloc(&plan->dev, plan->bytes);
         if (e != hipSuccess) {
             (void)hipHostFree(plan->pinned);
@@ -138,6 +134,14 @@ MSTAR_EXPORT size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan) {
 MSTAR_EXPORT int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const void* k_pages,
                                 const void* v_pages, const int32_t* block_table, void* out, float* lse,
                                 void* workspace, size_t workspace_bytes, void* stream) {
+    return mstar_attn_fwd_timed(plan, q, k_pages, v_pages, block_table, out, lse, workspace, workspace_bytes,
+                                stream, nullptr, nullptr);
+}
+
+MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, const void* k_pages,
+                                      const void* v_pages, const int32_t* block_table, void* out, float* lse,
+                                      void* workspace, size_t workspace_bytes, void* stream,
+                                      void* const* events_before, void* const* events_after) {
     if (!plan) return fail(MSTAR_ERR_INVALID_ARG, "plan is NULL");
     if (!plan->dev) return fail(MSTAR_ERR_INVALID_ARG, "plan was built host-only");
     const mstar::HostPlan& h = plan->host;
@@ -168,8 +172,6 @@ MSTAR_EXPORT int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const v
                                                      align256((size_t)h.partial_slots * D * sizeof(float)))
                           : nullptr;
     a.err = reinterpret_cast<int32_t*>(blob + plan->off_err);
-    a.units = reinterpret_cast<const mstar::SplitUnit*>(blob + plan->off_units);
-    a.counters = reinterpret_cast<int32_t*>(blob + plan->off_counters);
     a.hq = h.params.num_qo_heads;
     a.hkv = h.params.num_kv_heads;
     a.group = h.group;
@@ -180,20 +182,33 @@ MSTAR_EXPORT int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const v
     hipStream_t s = static_cast<hipStream_t>(stream);
 
     hipError_t e;
+    // optional HIP events around kernel class k (0 tiles, 1 few-row, 2 fp32, 3 merge)
+    auto mark = [&](void* const* evs, int k) -> hipError_t {
+        if (!evs || !evs[k]) return hipSuccess;
+        return hipEventRecord(static_cast<hipEvent_t>(evs[k]), s);
+    };
+#define MSTAR_MARK(evs, k) \
+    if ((e = mark(evs, k)) != hipSuccess) return hip_fail(e, "hipEventRecord")
     if (!h.tiles.empty()) {
         a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_tiles);
         a.n_items = (int32_t)h.tiles.size();
+        MSTAR_MARK(events_before, 0);
         if ((e = mstar::launch_tiles(a, D, s)) != hipSuccess) return hip_fail(e, "tile kernel launch");
+        MSTAR_MARK(events_after, 0);
     }
     if (!h.few.empty()) {
         a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_few);
         a.n_items = (int32_t)h.few.size();
+        MSTAR_MARK(events_before, 1);
         if ((e = mstar::launch_few(a, D, h.decode_rb, s)) != hipSuccess) return hip_fail(e, "few-row kernel launch");
+        MSTAR_MARK(events_after, 1);
     }
     if (!h.f32.empty()) {
         a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_f32);
         a.n_items = (int32_t)h.f32.size();
+        MSTAR_MARK(events_before, 2);
         if ((e = mstar::launch_f32(a, D, s)) != hipSuccess) return hip_fail(e, "fp32 kernel launch");
+        MSTAR_MARK(events_after, 2);
     }
     if (!h.merges.empty()) {
         mstar::MArgs m{};
@@ -204,9 +219,12 @@ MSTAR_EXPORT int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const v
         m.lse = lse;
         m.n_items = (int32_t)h.merges.size();
         m.hq = a.hq;
+        MSTAR_MARK(events_before, 3);
         if ((e = mstar::launch_merge(m, D, h.params.dtype == MSTAR_DTYPE_BF16, s)) != hipSuccess)
             return hip_fail(e, "merge kernel launch");
+        MSTAR_MARK(events_after, 3);
     }
+#undef MSTAR_MARK
     return MSTAR_OK;
 }
 
@@ -238,7 +256,7 @@ MSTAR_EXPORT int mstar_attn_plan_stats(const mstar_plan_t* plan, mstar_plan_stat
     out->prefill_items = (int64_t)h.tiles.size();
     out->decode_items = (int64_t)h.few.size();
     out->f32_items = (int64_t)h.f32.size();
-    out->merge_rows = h.merged_rows;
+    out->merge_rows = (int64_t)h.merges.size();
     out->partial_slots = h.partial_slots;
     out->total_q = h.total_q;
     out->plan_host_us = plan->plan_us;
@@ -266,8 +284,7 @@ MSTAR_EXPORT int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, i
         case 1: src = h.few.data(); n = h.few.size(); break;
         case 2: src = h.f32.data(); n = h.f32.size(); break;
         case 3: src = h.merges.data(); n = h.merges.size(); break;
-        case 4: src = h.units.data(); n = h.units.size(); break;
-        default: return fail(MSTAR_ERR_INVALID_ARG, "kind must be 0..4");
+        default: return fail(MSTAR_ERR_INVALID_ARG, "kind must be 0..3");
     }
     *count = (int64_t)n;
     if (capacity > 0 && !items) return fail(MSTAR_ERR_INVALID_ARG, "items is NULL");

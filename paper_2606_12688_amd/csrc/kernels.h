@@ -20,8 +20,6 @@ struct KArgs {
     float* part_o;    // [partial_slots][head_dim] fp32
     float* part_lse;  // [partial_slots] fp32 natural log
     int32_t* err;     // sticky device error word
-    const SplitUnit* units;  // split few-row units
-    int32_t* counters;       // per split unit: chunks finished (returns to 0)
     int32_t n_items;
     int32_t hq, hkv, group, bt_stride, num_pages;
     float sm_scale;

@@ -30,6 +30,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr int MSTAR_DEVERR_PAGE_RANGE_BIT = 1;  // MSTAR_DEVERR_PAGE_RANGE
 constexpr float kNegInf = -__builtin_inff();
 
 __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
@@ -361,40 +362,81 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
         for (int db = 0; db < DB; ++db) o[rb][db] = f32x4{0, 0, 0, 0};
     }
 
+    // Wave w takes steps w, w+4, w+8, ... of 32 keys; its i-th step starts at
+    // key k_begin + 32 * (w + 4 i) and spans exactly two pages (k_begin is page
+    // aligned).  The page indices of 32 consecutive steps live in one register
+    // (lane 2i+h holds half h of step i) and are read back with readlane, so no
+    // block-table load sits between a step and its K/V loads.
+    const int n_steps = (it.k_end - it.k_begin + SK - 1) / SK;
+    const int my_steps = wave < n_steps ? (n_steps - wave + 3) / 4 : 0;
+    const int32_t page0 = it.k_begin >> 4;
+    const int32_t n_pages = ((it.k_end + 15) >> 4) - page0;
+    auto load_pages = [&](int first_step) {
+        const int pg = 2 * (wave + 4 * (first_step + (lane >> 1))) + (lane & 1);
+        return pg < n_pages ? bt_row[page0 + pg] : 0;
+    };
+    int32_t pw_cur = load_pages(0), pw_next = my_steps > 32 ? load_pages(32) : 0;
+    const int64_t slot_stride = (int64_t)a.hkv * D;
+
+    // Loads are issued unconditionally from in-pool addresses (a key past the
+    // item's end, or on a page outside the pool, reads some valid slot) and a
+    // per-lane mask marks the rows to zero at compute time: predicated loads
+    // would make the compiler wait for every outstanding load.
     struct Step {
         uint4 k[2][DS];
         uint4 v[VL];
+        uint32_t dead;  // bit kb: K row kb of this lane; bit 2+j: V chunk j
     };
-    auto load_step = [&](Step& st, int32_t k0) {
+    bool page_err = false;
+    auto load_step = [&](Step& st, int i) {
+        if (i > 0 && (i & 31) == 0) {  // next window of page indices
+            pw_cur = pw_next;
+            pw_next = i + 32 < my_steps ? load_pages(i + 32) : 0;
+        }
+        const int32_t k0 = it.k_begin + SK * (wave + 4 * i);
+        int64_t base[2];
+        bool ok[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int32_t page = __builtin_amdgcn_readlane(pw_cur, 2 * (i & 31) + h);
+            ok[h] = (uint32_t)page < (uint32_t)a.num_pages;
+            page_err |= !ok[h] && k0 + 16 * h < it.k_end;
+            base[h] = ((int64_t)(ok[h] ? page : 0) * 16) * slot_stride + (int64_t)kvh * D;
+        }
+        uint32_t dead = 0;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-            const int32_t t = k0 + kb * 16 + n;
-            int64_t off = -1;
-            if (t < it.k_end) off = kv_offset(a, bt_row, t, kvh, D);
+            dead |= (!ok[kb] || k0 + kb * 16 + n >= it.k_end) ? (1u << kb) : 0u;
+            const int64_t off = base[kb] + n * slot_stride;
 #pragma unroll
-            for (int s = 0; s < DS; ++s)
-                st.k[kb][s] = off >= 0 ? load16(a.k, off + 32 * s + 8 * grp) : uint4{0, 0, 0, 0};
+            for (int s = 0; s < DS; ++s) st.k[kb][s] = load16(a.k, off + 32 * s + 8 * grp);
         }
 #pragma unroll
         for (int j = 0; j < VL; ++j) {
             const int c = lane + 64 * j;
             const int row = c / CH, col = (c % CH) * 8;
-            const int32_t t = k0 + row;
-            int64_t off = -1;
-            if (t < it.k_end) off = kv_offset(a, bt_row, t, kvh, D);
-            st.v[j] = off >= 0 ? load16(a.v, off + col) : uint4{0, 0, 0, 0};
+            const int h = row >> 4;
+            dead |= (!ok[h] || k0 + row >= it.k_end) ? (4u << j) : 0u;
+            st.v[j] = load16(a.v, base[h] + (row & 15) * slot_stride + col);
         }
+        st.dead = dead;
+    };
+    auto zero_dead = [&](Step& st) {
+        if (__builtin_amdgcn_ballot_w64(st.dead != 0) == 0) return;  // wave-uniform: usually nothing to do
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int s = 0; s < DS; ++s)
+                if (st.dead & (1u << kb)) st.k[kb][s] = uint4{0, 0, 0, 0};
+#pragma unroll
+        for (int j = 0; j < VL; ++j)
+            if (st.dead & (4u << j)) st.v[j] = uint4{0, 0, 0, 0};
     };
 
     bf16_t* vst = v_lds[wave];
-    const int n_steps = (it.k_end - it.k_begin + SK - 1) / SK;
-    Step cur, nxt;
-    if (wave < n_steps) load_step(cur, it.k_begin + wave * SK);
-    for (int st = wave; st < n_steps; st += 4) {
-        const int32_t k0 = it.k_begin + st * SK;
-        const bool more = st + 4 < n_steps;
-        if (more) load_step(nxt, k0 + 4 * SK);
-
+    auto compute_step = [&](Step& cur, int i) {
+        const int32_t k0 = it.k_begin + SK * (wave + 4 * i);
+        zero_dead(cur);
         f32x4 sc[RB][2];
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) sc[rb][0] = sc[rb][1] = f32x4{0, 0, 0, 0};
@@ -423,11 +465,11 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int32_t key = k0 + kb * 16 + 4 * grp + i;
-                    float x = sc[rb][kb][i] * a.scale_log2;
+                for (int e = 0; e < 4; ++e) {
+                    const int32_t key = k0 + kb * 16 + 4 * grp + e;
+                    float x = sc[rb][kb][e] * a.scale_log2;
                     if (!full && !(key >= lo[rb] && key < hi[rb])) x = kNegInf;
-                    sc[rb][kb][i] = x;
+                    sc[rb][kb][e] = x;
                 }
             const float alpha = softmax_update<2>(sc[rb], m[rb], l[rb]);
 #pragma unroll
@@ -444,8 +486,36 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
             for (int rb = 0; rb < RB; ++rb) o[rb][db] = mfma16(vf, pf[rb], o[rb][db]);
         }
         asm volatile("" ::: "memory");
-        if (more) cur = nxt;
+    };
+
+    // Two register buffers: step i computes while step i+1 (and then i+2) is in
+    // flight.  The steady-state loop always issues both loads, so every path
+    // into it has the same loads pending and the compiler waits only for the
+    // buffer it is about to use; the last two or three steps are peeled.
+    Step sa, sb;
+    int i = 0;
+    if (my_steps >= 4) {
+        load_step(sa, 0);
+        load_step(sb, 1);
+        do {
+            compute_step(sa, i);
+            load_step(sa, i + 2);
+            compute_step(sb, i + 1);
+            load_step(sb, i + 3);
+            i += 2;
+        } while (i + 3 < my_steps);
+    } else {
+        if (my_steps > 0) load_step(sa, 0);
+        if (my_steps > 1) load_step(sb, 1);
     }
+    if (i < my_steps) {
+        compute_step(sa, i);
+        if (i + 2 < my_steps) load_step(sa, i + 2);
+    }
+    if (i + 1 < my_steps) compute_step(sb, i + 1);
+    if (i + 2 < my_steps) compute_step(sa, i + 2);
+
+    if (page_err && lane == 0) atomicOr(a.err, MSTAR_DEVERR_PAGE_RANGE_BIT);
 
     // ---- combine the four waves -------------------------------------------------
     float lt[RB];
@@ -511,43 +581,6 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
             if (d4 == 0) a.part_lse[slot] = lse;
         }
     }
-    if (it.unit < 0) return;
-
-    // ---- split unit: the last chunk to finish merges the unit's partials ------
-    __shared__ int is_last;
-    __threadfence();  // release: this chunk's partials are visible device-wide
-    __syncthreads();
-    if (tid == 0) {
-        const int prev = atomicAdd(&a.counters[it.unit], 1);
-        is_last = prev == a.units[it.unit].nch - 1;
-    }
-    __syncthreads();
-    if (!is_last) return;
-    __threadfence();  // acquire: see every other chunk's partials
-    const SplitUnit u = a.units[it.unit];
-    for (int e = tid; e < NV; e += 256) {
-        const int row = e / (D / 4), d4 = (e % (D / 4)) * 4;
-        if (row >= u.rows) continue;
-        float mstar = kNegInf;
-        for (int c = 0; c < u.nch; ++c) mstar = fmaxf(mstar, a.part_lse[u.slot0 + (int64_t)c * u.rows + row]);
-        f32x4 acc = {0, 0, 0, 0};
-        float tot = 0.0f;
-        if (mstar != kNegInf) {
-            for (int c = 0; c < u.nch; ++c) {
-                const int64_t slot = u.slot0 + (int64_t)c * u.rows + row;
-                const float w = expf(a.part_lse[slot] - mstar);
-                tot += w;
-                acc += w * *reinterpret_cast<const f32x4*>(a.part_o + slot * D + d4);
-            }
-        }
-        const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
-        const int rr = u.row0 + row;
-        const int64_t orow = (int64_t)(si.q_start + rr / G) * a.hq + u.head * G + rr % G;
-        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16_t*>(a.out) + orow * D + d4) =
-            __builtin_convertvector(acc * inv, bf16x4);
-        if (d4 == 0) a.lse[orow] = tot > 0.0f ? mstar + logf(tot) : kNegInf;
-    }
-    if (tid == 0) atomicExch(&a.counters[it.unit], 0);  // ready for the next call
 }
 
 // ---------------------------------------------------------------------------

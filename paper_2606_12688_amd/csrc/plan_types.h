@@ -26,18 +26,10 @@ struct SeqInfo {
 //  few-row items: `head` is a KV head; row r in [row0, row0+nrows) stands for
 //    query row r / G and query head head*G + r % G (G = Hq / Hkv).
 // part < 0: write the final out/lse; otherwise write fp32 partials to slots
-// part + (r - row0).  unit >= 0 (few-row items only): the item is one chunk of
-// split unit `unit`; the last chunk to finish merges the unit's partials.
+// part + (r - row0), combined afterwards by the merge kernel.
 struct WorkItem {
     int32_t seq, head, row0, nrows;
-    int32_t k_begin, k_end, part, unit;
-};
-
-// A few-row unit whose key range is split into nch chunks: chunk c writes row
-// r's partial to slot slot0 + c * rows + r.
-struct SplitUnit {
-    int32_t slot0, nch, rows, seq;
-    int32_t head, row0, pad0, pad1;
+    int32_t k_begin, k_end, part, unit;  // unit: reserved, -1
 };
 
 // Output (packed_row, head) assembled from nslots partials at
@@ -50,6 +42,5 @@ struct MergeItem {
 static_assert(sizeof(SeqInfo) == 32, "SeqInfo layout");
 static_assert(sizeof(WorkItem) == 32, "WorkItem layout");
 static_assert(sizeof(MergeItem) == 32, "MergeItem layout");
-static_assert(sizeof(SplitUnit) == 32, "SplitUnit layout");
 
 }  // namespace mstar

@@ -27,6 +27,16 @@
 #include <cmath>
 #include <cstdio>
 
+// Few-row key chunks are sized to total_keys / MSTAR_FEW_TARGET_ITEMS (at least
+// 256 keys), which with per-unit rounding gives about 1.2-1.3x that many items:
+// a little over one round of the 512 workgroup slots of 256 CUs, enough for
+// the longest-first order to balance ragged lengths.  Every split item costs
+// an fp32 partial write and read-back in the merge kernel, so fewer is better
+// once the GPU is full (measured on the decode batch: 512 beats 1024 and 2048).
+#ifndef MSTAR_FEW_TARGET_ITEMS
+#define MSTAR_FEW_TARGET_ITEMS 512
+#endif
+
 namespace mstar {
 namespace {
 
@@ -255,22 +265,10 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             w.k_begin = (int32_t)(u.k_begin + c * cs);
             w.k_end = (int32_t)std::min<int64_t>(u.k_begin + (c + 1) * cs, u.k_end);
             w.part = nch > 1 ? (int32_t)(slot + c * u.nrows) : -1;
-            w.unit = (nch > 1 && few) ? (int32_t)plan.units.size() : -1;
+            w.unit = -1;
             dst.push_back(w);
         }
-        if (nch > 1) plan.merged_rows += u.nrows;
-        if (nch > 1 && few) {
-            SplitUnit su;
-            su.slot0 = (int32_t)slot;
-            su.nch = (int32_t)nch;
-            su.rows = u.nrows;
-            su.seq = u.seq;
-            su.head = u.head;
-            su.row0 = u.row0;
-            su.pad0 = su.pad1 = 0;
-            plan.units.push_back(su);
-            slot += nch * u.nrows;
-        } else if (nch > 1) {
+        if (nch > 1) {
             const SeqInfo& si = plan.seqs[u.seq];
             for (int32_t r = 0; r < u.nrows; ++r) {
                 MergeItem m;
@@ -294,7 +292,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         if (P.flags & MSTAR_FLAG_FORCE_SPLIT) {
             chunk = kSubKeys * 2;
         } else if (!(P.flags & MSTAR_FLAG_NO_SPLIT)) {
-            const int64_t target_items = 2048;
+            const int64_t target_items = MSTAR_FEW_TARGET_ITEMS;
             int64_t c = std::max<int64_t>(256, ceil_div(total, target_items));
             chunk = (int32_t)std::min<int64_t>(ceil_div(c, 128) * 128, INT32_MAX / 2);
         }

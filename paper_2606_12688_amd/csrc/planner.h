@@ -6,7 +6,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/mstar_attn.h"
+#include "mstar_attn.h"
 #include "plan_types.h"
 
 namespace mstar {
@@ -23,9 +23,7 @@ struct HostPlan {
     std::vector<WorkItem> tiles;          // multi-row kernel
     std::vector<WorkItem> few;            // few-row kernel
     std::vector<WorkItem> f32;            // fp32 kernel
-    std::vector<MergeItem> merges;        // merged by the merge kernel (split tiles)
-    std::vector<SplitUnit> units;         // split few-row units (merged in-kernel)
-    int64_t merged_rows = 0;              // (row, head) outputs assembled from partials
+    std::vector<MergeItem> merges;        // (row, head) outputs assembled from partials
     int64_t visible_pairs = 0;
     int64_t partial_slots = 0;
 };

@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import workloads as W
-from oracle import attend, block_ids, merge_partials, oracle_attention, visible_matrix
+from oracle import attend, block_ids, merge_partials, oracle_attention, oracle_rows, visible_matrix
 from oracle.scalar import scalar_attention
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -264,3 +264,18 @@ def test_split_and_merge_equals_unsplit(seed):
     # all chunks empty for a row -> zero / -inf
     mo2, ml2 = merge_partials([np.ones((1, 2))] * 2, [np.array([-np.inf])] * 2)
     assert np.all(mo2 == 0) and np.isneginf(ml2[0])
+
+
+def test_sampled_rows_agree_with_scalar_oracle():
+    b = W.reduced("tiny_causal_f32")
+    segs = [[(0, 9, 0, 0), (9, 20, 2, 6), (29, 6, 1, 0)], [(0, 12, 0, 0)]]
+    bt = np.array([[3, 0, 4], [1, 2, -1]], dtype=np.int32)
+    b = W._finish("t", 4, 2, 8, "f32", [30, 5], [35, 12], segs, [0, 4], bt, 5, 0)
+    t = W.make_tensors_numpy(b)
+    so, sl = scalar_attention(b, t["q"].tolist(), t["k_pages"].tolist(), t["v_pages"].tolist())
+    picks = [(0, 0, 0), (0, 11, 3), (0, 29, 1), (1, 0, 2), (1, 4, 0)]
+    ro, rl = oracle_rows(b, t["q"], t["k_pages"], t["v_pages"], picks)
+    for n, (r, i, h) in enumerate(picks):
+        row = int(b.seqs[r, 2]) + i
+        np.testing.assert_allclose(ro[n], so[row][h], rtol=0, atol=1e-12)
+        assert abs(rl[n] - sl[row][h]) < 1e-12
