@@ -107,7 +107,7 @@ typedef struct {
     int32_t max_blocks_per_seq; /* row stride of block_table; kv_len <= 16 * this */
     int32_t num_pages;          /* pages in the pool (bounds-checked on device)   */
     uint32_t flags;             /* MSTAR_FLAG_*                                   */
-    float sm_scale;             /* score scale, typically 1/sqrt(head_dim)        */
+    float sm_scale;             /* score scale > 0, typically 1/sqrt(head_dim)    */
 } mstar_attn_params;
 
 typedef struct mstar_plan mstar_plan_t;

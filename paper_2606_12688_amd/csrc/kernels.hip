@@ -39,17 +39,30 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Reductions over the four lanes l, l^16, l^32, l^48 that share a query row.
-__device__ __forceinline__ float rowgroup_max(float x) {
-    x = fmaxf(x, __shfl_xor(x, 16, 64));
-    x = fmaxf(x, __shfl_xor(x, 32, 64));
-    return x;
-}
-__device__ __forceinline__ float rowgroup_sum(float x) {
-    x += __shfl_xor(x, 16, 64);
-    x += __shfl_xor(x, 32, 64);
-    return x;
-}
+// Reductions over the four lanes l, l^16, l^32, l^48 that share a query row,
+// with gfx950's permlane swaps (v_permlane32_swap exchanges the upper half-wave
+// of one register with the lower half of another; with both operands the same
+// value, the two results hold x[l] and x[l^32] in some order, and likewise
+// for 16).  Sums are formed in the same order on all four lanes.
+struct RowGroup {
+    __device__ __forceinline__ static float max(float x) {
+        const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+        const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+    }
+    __device__ __forceinline__ static float sum(float x) {
+        const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+        const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+    }
+};
+
+// Workgroup barrier for LDS hand-offs: waits for this wave's LDS (and scalar)
+// operations only, so global loads into registers stay in flight across it
+// (__syncthreads also waits for every outstanding global load).
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 __device__ __forceinline__ bf16x4 lds_read_tr16(const bf16_t* p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
@@ -75,6 +88,21 @@ __device__ __forceinline__ int64_t kv_offset(const KArgs& a, const int32_t* bt_r
     return (((int64_t)page * 16 + (t & 15)) * a.hkv + kvh) * D;
 }
 
+// K/V rows are read through a buffer resource per page: the page base lives in
+// scalar registers (built with scalar ops from the wave-uniform page index) and
+// each lane adds a 32-bit byte offset that does not change from tile to tile,
+// so the loads cost no vector ALU work.  The resource's range is one page.
+constexpr int kBufferDword3 = 0x00020000;  // gfx9 buffer resource word 3 (raw, no format)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t page_rsrc(const char* base, size_t byte_ofs, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base + byte_ofs), (short)0, (int)bytes,
+                                             kBufferDword3);
+}
+
+__device__ __forceinline__ uint4 load16_at(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, 0));
+}
+
 __device__ __forceinline__ uint4 load16(const void* base, int64_t elem_off_bf16) {
     return *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(base) + elem_off_bf16);
 }
@@ -89,31 +117,49 @@ __device__ __forceinline__ void row_interval(const KArgs& a, const SeqInfo& si, 
     hi = min(h0, it.k_end);
 }
 
-// Online-softmax update of one 16-row block with NB 16-key blocks of scores
-// (already scaled to base 2 and masked).  Returns the rescale factor for O.
+// Online-softmax update of one 16-row block with NB 16-key blocks of raw
+// scores (hidden keys already -inf).  m and l are kept in base-2 units of the
+// scaled scores: c = sm_scale * log2(e) > 0, so max(c s) = c max(s) and every
+// probability is one FMA and one exp2.
+//
+// The reference max m is refreshed lazily: only when some row of the wave
+// sees its max grow by more than kLazy (or has no reference yet).  Otherwise
+// probabilities are taken against the stale m, so they stay below 2^kLazy, and
+// the rescale of the O accumulators (the most expensive VALU work per tile)
+// is skipped.  The result is exact either way: out = O / l and
+// lse = m + log2(l) use the same reference.  Returns true (wave-uniform) when
+// O must be multiplied by `alpha`.  Leaves the probabilities in s.
+constexpr float kLazy = 8.0f;
+
 template <int NB>
-__device__ __forceinline__ float softmax_update(f32x4 (&s)[NB], float& m, float& l) {
+__device__ __forceinline__ bool softmax_update(const RowGroup& rg, f32x4 (&s)[NB], float c, float& m, float& l,
+                                               float& alpha) {
     float mx = kNegInf;
 #pragma unroll
     for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kb][i]);
-    mx = rowgroup_max(mx);
-    const float m_new = fmaxf(m, mx);
-    const float m_use = m_new == kNegInf ? 0.0f : m_new;
-    const float alpha = fast_exp2(m - m_use);
+    mx = rg.max(mx) * c;
+    const bool grow = mx > m + kLazy;  // false while both are -inf
+    const bool rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
+    alpha = 1.0f;
+    if (rescale) {
+        const float m_new = fmaxf(m, mx);
+        alpha = fast_exp2(m - (m_new == kNegInf ? 0.0f : m_new));
+        m = m_new;
+    }
+    const float m_use = m == kNegInf ? 0.0f : m;
     float sum = 0.0f;
 #pragma unroll
     for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float p = fast_exp2(s[kb][i] - m_use);
+            const float p = fast_exp2(fmaf(s[kb][i], c, -m_use));
             s[kb][i] = p;
             sum += p;
         }
-    l = l * alpha + sum;  // per-lane partial sum; the row total is reduced at the end
-    m = m_new;
-    return alpha;
+    l = rescale ? l * alpha + sum : l + sum;  // per-lane partial; row total reduced at the end
+    return rescale;
 }
 
 // ---------------------------------------------------------------------------
@@ -139,6 +185,7 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
     const int n = lane & 15, grp = lane >> 4;
     const int kvh = it.head / a.group;
     const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
+    const RowGroup rg;
 
     // ---- rows owned by this lane ------------------------------------------
     int32_t lo[2], hi[2];
@@ -179,22 +226,62 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
 #pragma unroll
         for (int db = 0; db < DB; ++db) o[rb][db] = f32x4{0, 0, 0, 0};
 
+    // Page indices of 64 consecutive pages (16 tiles) of the item sit in one
+    // register per wave (lane i = page i of the window) and are read back with
+    // readlane: the rows a thread loads share a page across the wave, so no
+    // block-table load stands between a tile and its K/V loads.  Loads are
+    // issued unconditionally from in-pool addresses; rows past the item's end
+    // (or on a page outside the pool) are zeroed when stored to LDS.
+    const int32_t page0 = it.k_begin >> 4;
+    const int32_t n_pages = ((it.k_end + 15) >> 4) - page0;
+    auto load_pages = [&](int first) {
+        const int pg = first + lane;
+        return pg < n_pages ? bt_row[page0 + pg] : 0;
+    };
+    int32_t pw_cur = load_pages(0), pw_next = n_pages > 64 ? load_pages(64) : 0;
+    int win = 0;
+    bool page_err = false;
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int64_t slot_stride = (int64_t)a.hkv * D;
+    const size_t page_bytes = (size_t)16 * slot_stride * sizeof(bf16_t);
+    constexpr int PPT = BN / 16;  // pages per tile
+    // byte offset of each of this thread's rows inside its page: the same for every tile
+    uint32_t toff[LOADS];
+#pragma unroll
+    for (int j = 0; j < LOADS; ++j) {
+        const int c = tid + 256 * j;
+        const int row = c / CH, col = (c % CH) * 8;
+        toff[j] = (uint32_t)((((row & 15) * slot_stride) + (int64_t)kvh * D + col) * sizeof(bf16_t));
+    }
+    const char* kbase = reinterpret_cast<const char*>(a.k);
+    const char* vbase = reinterpret_cast<const char*>(a.v);
     uint4 kreg[LOADS], vreg[LOADS];
-    auto load_tile = [&](int32_t k0) {
+    // Rows past the item's end read zeros through the buffer range check (their
+    // offset is pushed past the page), and a page outside the pool gets an
+    // empty range: no selects on the data and no access outside the pool.
+    constexpr uint32_t kOutOfRange = 0x80000000u;
+    auto load_tile = [&](int tix) {
+        const int rel0 = tix * PPT;
+        if ((rel0 >> 6) != win) {  // next window of page indices
+            ++win;
+            pw_cur = pw_next;
+            pw_next = 64 * (win + 1) < n_pages ? load_pages(64 * (win + 1)) : 0;
+        }
+        const int32_t k0 = it.k_begin + tix * BN;
+        const bool tail = k0 + BN > it.k_end;
 #pragma unroll
         for (int j = 0; j < LOADS; ++j) {
-            const int c = tid + 256 * j;
-            const int row = c / CH, col = (c % CH) * 8;
-            const int32_t t = k0 + row;
-            kreg[j] = uint4{0, 0, 0, 0};
-            vreg[j] = uint4{0, 0, 0, 0};
-            if (t < it.k_end) {
-                const int64_t off = kv_offset(a, bt_row, t, kvh, D);
-                if (off >= 0) {
-                    kreg[j] = load16(a.k, off + col);
-                    vreg[j] = load16(a.v, off + col);
-                }
-            }
+            // page of this row within the tile: the same for the whole wave
+            const int pg = (wave_u * 64 / CH) / 16 + (256 / CH / 16) * j;
+            const int32_t page = __builtin_amdgcn_readlane(pw_cur, (rel0 + pg) & 63);
+            const bool ok = (uint32_t)page < (uint32_t)a.num_pages;
+            page_err |= !ok && k0 + 16 * pg < it.k_end;
+            const size_t pofs = ok ? (size_t)page * page_bytes : 0;
+            const uint32_t nrec = ok ? (uint32_t)page_bytes : 0u;
+            uint32_t off = toff[j];
+            if (tail) off = k0 + (tid + 256 * j) / CH < it.k_end ? off : kOutOfRange;
+            kreg[j] = load16_at(page_rsrc(kbase, pofs, nrec), off);
+            vreg[j] = load16_at(page_rsrc(vbase, pofs, nrec), off);
         }
     };
     auto store_tile = [&](int buf) {
@@ -207,71 +294,81 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
         }
     };
 
+    const float c2 = a.scale_log2;
     const int n_tiles = (it.k_end - it.k_begin + BN - 1) / BN;
-    load_tile(it.k_begin);
+    load_tile(0);
     store_tile(0);
-    __syncthreads();
+    load_tile(min(1, n_tiles - 1));
+    lds_barrier();
 
+    // one tile of K/V loads in flight while the previous tile is computed; the
+    // last tiles reload the final tile so the loop body stays uniform
     for (int tix = 0; tix < n_tiles; ++tix) {
         const int32_t k0 = it.k_begin + tix * BN;
         const int buf = tix & 1;
-        const bool more = tix + 1 < n_tiles;
-        if (more) load_tile(k0 + BN);
 
         if (wave_active && k0 < w_hi_max && k0 + BN > w_lo_min) {
             const bool full = k0 >= w_lo_max && k0 + BN <= w_hi_min;
             f32x4 sc[2][4];
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb)
-#pragma unroll
-                for (int kb = 0; kb < 4; ++kb) sc[rb][kb] = f32x4{0, 0, 0, 0};
-#pragma unroll
             for (int kb = 0; kb < 4; ++kb) {
+                bf16x8 kf[DS];
 #pragma unroll
-                for (int s = 0; s < DS; ++s) {
-                    const bf16x8 kf = *reinterpret_cast<const bf16x8*>(
-                        &k_lds[buf][(kb * 16 + n) * KS + 32 * s + 8 * grp]);
+                for (int s = 0; s < DS; ++s)
+                    kf[s] = *reinterpret_cast<const bf16x8*>(&k_lds[buf][(kb * 16 + n) * KS + 32 * s + 8 * grp]);
 #pragma unroll
-                    for (int rb = 0; rb < 2; ++rb) sc[rb][kb] = mfma16(kf, qf[rb][s], sc[rb][kb]);
-                }
+                for (int rb = 0; rb < 2; ++rb) sc[rb][kb] = mfma16(kf[0], qf[rb][0], f32x4{0, 0, 0, 0});
+#pragma unroll
+                for (int s = 1; s < DS; ++s)
+#pragma unroll
+                    for (int rb = 0; rb < 2; ++rb) sc[rb][kb] = mfma16(kf[s], qf[rb][s], sc[rb][kb]);
             }
 #pragma unroll
             for (int rb = 0; rb < 2; ++rb) {
+                if (!full) {
+                    // key k0 + 4 grp + c is visible iff lo <= key < hi
+                    const int32_t lo_r = lo[rb] - (k0 + 4 * grp), hi_r = hi[rb] - (k0 + 4 * grp);
 #pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
+                    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int32_t key = k0 + kb * 16 + 4 * grp + i;
-                        float x = sc[rb][kb][i] * a.scale_log2;
-                        if (!full && !(key >= lo[rb] && key < hi[rb])) x = kNegInf;
-                        sc[rb][kb][i] = x;
-                    }
-                const float alpha = softmax_update<4>(sc[rb], m[rb], l[rb]);
+                        for (int i = 0; i < 4; ++i) {
+                            const int c = kb * 16 + i;
+                            if (!(c >= lo_r && c < hi_r)) sc[rb][kb][i] = kNegInf;
+                        }
+                }
+                float alpha;
+                if (softmax_update<4>(rg, sc[rb], c2, m[rb], l[rb], alpha)) {
 #pragma unroll
-                for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+                    for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+                }
             }
 #pragma unroll
             for (int c = 0; c < 2; ++c) {
                 bf16x8 pf[2];
 #pragma unroll
                 for (int rb = 0; rb < 2; ++rb) pf[rb] = to_bf16x8(sc[rb][2 * c], sc[rb][2 * c + 1]);
+                bf16x8 vf[DB];
 #pragma unroll
                 for (int db = 0; db < DB; ++db) {
                     const bf16_t* base = &v_lds[buf][(32 * c + 4 * grp + (n >> 2)) * VS + db * 16 + (n & 3) * 4];
-                    const bf16x8 vf = cat(lds_read_tr16(base), lds_read_tr16(base + 16 * VS));
-#pragma unroll
-                    for (int rb = 0; rb < 2; ++rb) o[rb][db] = mfma16(vf, pf[rb], o[rb][db]);
+                    vf[db] = cat(lds_read_tr16(base), lds_read_tr16(base + 16 * VS));
                 }
+#pragma unroll
+                for (int db = 0; db < DB; ++db)
+#pragma unroll
+                    for (int rb = 0; rb < 2; ++rb) o[rb][db] = mfma16(vf[db], pf[rb], o[rb][db]);
             }
         }
-        if (more) store_tile(buf ^ 1);
-        __syncthreads();
+        store_tile(buf ^ 1);
+        load_tile(min(tix + 2, n_tiles - 1));
+        lds_barrier();
     }
+    if (page_err && lane == 0) atomicOr(a.err, MSTAR_DEVERR_PAGE_RANGE_BIT);
 
     // ---- epilogue -------------------------------------------------------------
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
-        const float lt = rowgroup_sum(l[rb]);
+        const float lt = rg.sum(l[rb]);
         if (!valid[rb]) continue;
         const int r = wave * 32 + rb * 16 + n;
         const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
@@ -322,6 +419,7 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
     const int G = a.group;
     const int kvh = it.head;
     const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
+    const RowGroup rg;
 
     int32_t lo[RB], hi[RB];
     bool valid[RB];
@@ -385,8 +483,25 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
     struct Step {
         uint4 k[2][DS];
         uint4 v[VL];
-        uint32_t dead;  // bit kb: K row kb of this lane; bit 2+j: V chunk j
     };
+    // Byte offsets of this lane's K and V chunks inside their page, the same
+    // for every step; the page (wave-uniform) supplies a scalar base.  Rows past
+    // the item's end read zeros through the buffer range check and a page
+    // outside the pool gets an empty range, so the data needs no selects.
+    constexpr uint32_t kOutOfRange = 0x80000000u;
+    const size_t page_bytes = (size_t)16 * slot_stride * sizeof(bf16_t);
+    uint32_t koff[DS], voff[VL];
+#pragma unroll
+    for (int s = 0; s < DS; ++s)
+        koff[s] = (uint32_t)((n * slot_stride + (int64_t)kvh * D + 32 * s + 8 * grp) * sizeof(bf16_t));
+#pragma unroll
+    for (int j = 0; j < VL; ++j) {
+        const int c = lane + 64 * j;
+        const int row = c / CH, col = (c % CH) * 8;
+        voff[j] = (uint32_t)(((row & 15) * slot_stride + (int64_t)kvh * D + col) * sizeof(bf16_t));
+    }
+    const char* kbase = reinterpret_cast<const char*>(a.k);
+    const char* vbase = reinterpret_cast<const char*>(a.v);
     bool page_err = false;
     auto load_step = [&](Step& st, int i) {
         if (i > 0 && (i & 31) == 0) {  // next window of page indices
@@ -394,59 +509,45 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
             pw_next = i + 32 < my_steps ? load_pages(i + 32) : 0;
         }
         const int32_t k0 = it.k_begin + SK * (wave + 4 * i);
-        int64_t base[2];
-        bool ok[2];
+        const bool tail = k0 + SK > it.k_end;
+        __amdgpu_buffer_rsrc_t rk[2], rv[2];
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int32_t page = __builtin_amdgcn_readlane(pw_cur, 2 * (i & 31) + h);
-            ok[h] = (uint32_t)page < (uint32_t)a.num_pages;
-            page_err |= !ok[h] && k0 + 16 * h < it.k_end;
-            base[h] = ((int64_t)(ok[h] ? page : 0) * 16) * slot_stride + (int64_t)kvh * D;
+            const bool ok = (uint32_t)page < (uint32_t)a.num_pages;
+            page_err |= !ok && k0 + 16 * h < it.k_end;
+            const size_t pofs = ok ? (size_t)page * page_bytes : 0;
+            const uint32_t nrec = ok ? (uint32_t)page_bytes : 0u;
+            rk[h] = page_rsrc(kbase, pofs, nrec);
+            rv[h] = page_rsrc(vbase, pofs, nrec);
         }
-        uint32_t dead = 0;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-            dead |= (!ok[kb] || k0 + kb * 16 + n >= it.k_end) ? (1u << kb) : 0u;
-            const int64_t off = base[kb] + n * slot_stride;
+            const bool live = !tail || k0 + kb * 16 + n < it.k_end;
 #pragma unroll
-            for (int s = 0; s < DS; ++s) st.k[kb][s] = load16(a.k, off + 32 * s + 8 * grp);
+            for (int s = 0; s < DS; ++s) st.k[kb][s] = load16_at(rk[kb], live ? koff[s] : kOutOfRange);
         }
 #pragma unroll
         for (int j = 0; j < VL; ++j) {
-            const int c = lane + 64 * j;
-            const int row = c / CH, col = (c % CH) * 8;
-            const int h = row >> 4;
-            dead |= (!ok[h] || k0 + row >= it.k_end) ? (4u << j) : 0u;
-            st.v[j] = load16(a.v, base[h] + (row & 15) * slot_stride + col);
+            const int row = (lane + 64 * j) / CH;
+            const int h = (64 * j / CH) >> 4;  // the chunk's page half: the same across the wave
+            const bool live = !tail || k0 + row < it.k_end;
+            st.v[j] = load16_at(rv[h], live ? voff[j] : kOutOfRange);
         }
-        st.dead = dead;
-    };
-    auto zero_dead = [&](Step& st) {
-        if (__builtin_amdgcn_ballot_w64(st.dead != 0) == 0) return;  // wave-uniform: usually nothing to do
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int s = 0; s < DS; ++s)
-                if (st.dead & (1u << kb)) st.k[kb][s] = uint4{0, 0, 0, 0};
-#pragma unroll
-        for (int j = 0; j < VL; ++j)
-            if (st.dead & (4u << j)) st.v[j] = uint4{0, 0, 0, 0};
     };
 
     bf16_t* vst = v_lds[wave];
     auto compute_step = [&](Step& cur, int i) {
         const int32_t k0 = it.k_begin + SK * (wave + 4 * i);
-        zero_dead(cur);
         f32x4 sc[RB][2];
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) sc[rb][0] = sc[rb][1] = f32x4{0, 0, 0, 0};
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int s = 0; s < DS; ++s) {
                 const bf16x8 kf = __builtin_bit_cast(bf16x8, cur.k[kb][s]);
 #pragma unroll
-                for (int rb = 0; rb < RB; ++rb) sc[rb][kb] = mfma16(kf, qf[rb][s], sc[rb][kb]);
+                for (int rb = 0; rb < RB; ++rb)
+                    sc[rb][kb] = mfma16(kf, qf[rb][s], s == 0 ? f32x4{0, 0, 0, 0} : sc[rb][kb]);
             }
         // stage V for the transpose read (wave-private slice; LDS executes a
         // wave's accesses in order, the asm keeps the compiler from reordering)
@@ -462,18 +563,21 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
         const bool full = k0 >= lo_max && k0 + SK <= hi_min;
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
+            if (!full) {
+                const int32_t lo_r = lo[rb] - (k0 + 4 * grp), hi_r = hi[rb] - (k0 + 4 * grp);
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+                for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int32_t key = k0 + kb * 16 + 4 * grp + e;
-                    float x = sc[rb][kb][e] * a.scale_log2;
-                    if (!full && !(key >= lo[rb] && key < hi[rb])) x = kNegInf;
-                    sc[rb][kb][e] = x;
-                }
-            const float alpha = softmax_update<2>(sc[rb], m[rb], l[rb]);
+                    for (int e = 0; e < 4; ++e) {
+                        const int c = kb * 16 + e;
+                        if (!(c >= lo_r && c < hi_r)) sc[rb][kb][e] = kNegInf;
+                    }
+            }
+            float alpha;
+            if (softmax_update<2>(rg, sc[rb], a.scale_log2, m[rb], l[rb], alpha)) {
 #pragma unroll
-            for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+                for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+            }
         }
         bf16x8 pf[RB];
 #pragma unroll
@@ -520,7 +624,7 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
     // ---- combine the four waves -------------------------------------------------
     float lt[RB];
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) lt[rb] = rowgroup_sum(l[rb]);
+    for (int rb = 0; rb < RB; ++rb) lt[rb] = rg.sum(l[rb]);
     __syncthreads();  // every wave is done with its V slice
     if (grp == 0) {
 #pragma unroll

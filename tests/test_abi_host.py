@@ -137,6 +137,9 @@ def _params(**kw):
     (dict(masks=[[0, 1, -3]]), attn.ERR_INVALID_ARG),          # negative window
     (dict(masks=[[0, 2, 0]]), attn.ERR_INVALID_ARG),           # segment range past the array
     (dict(max_blocks_per_seq=0), attn.ERR_INVALID_ARG),
+    (dict(sm_scale=0.0), attn.ERR_INVALID_ARG),
+    (dict(sm_scale=-0.5), attn.ERR_INVALID_ARG),
+    (dict(sm_scale=float("nan")), attn.ERR_INVALID_ARG),
     (dict(seqs=[[3, 70, 0]], segments=[[0, 70, 0, 0]]), attn.ERR_INVALID_ARG),  # kv_len > 16 * max_blocks
     (dict(seqs=[[3, 10, 0], [3, 10, 2]], masks=[[0, 1, 0], [0, 1, 0]]), attn.ERR_INVALID_ARG),  # rows overlap
     (dict(flags=attn.FLAG_HOST_ONLY | attn.FLAG_FORCE_SPLIT | attn.FLAG_NO_SPLIT), attn.ERR_INVALID_ARG),
