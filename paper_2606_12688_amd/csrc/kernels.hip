@@ -44,12 +44,17 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // of one register with the lower half of another; with both operands the same
 // value, the two results hold x[l] and x[l^32] in some order, and likewise
 // for 16).  Sums are formed in the same order on all four lanes.
+// IEEE maximumNumber: the hardware max instruction as is.  fmaxf also has to
+// quiet signalling NaNs, which costs an extra instruction per operand whenever
+// the compiler cannot prove an input is not one (e.g. after a masking select).
+__device__ __forceinline__ float fmax_num(float a, float b) { return __builtin_elementwise_maximumnum(a, b); }
+
 struct RowGroup {
     __device__ __forceinline__ static float max(float x) {
         const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-        x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+        x = fmax_num(__uint_as_float(a[0]), __uint_as_float(a[1]));
         const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-        return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+        return fmax_num(__uint_as_float(b[0]), __uint_as_float(b[1]));
     }
     __device__ __forceinline__ static float sum(float x) {
         const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -131,53 +136,141 @@ __device__ __forceinline__ void row_interval(const KArgs& a, const SeqInfo& si, 
 // O must be multiplied by `alpha`.  Leaves the probabilities in s.
 constexpr float kLazy = 8.0f;
 
+// Balanced reductions over the 4*NB score values a lane holds for one row.
 template <int NB>
-__device__ __forceinline__ bool softmax_update(const RowGroup& rg, f32x4 (&s)[NB], float c, float& m, float& l,
-                                               float& alpha) {
-    float mx = kNegInf;
+__device__ __forceinline__ float tree_max(const f32x4 (&s)[NB]) {
+    float v[NB];
 #pragma unroll
-    for (int kb = 0; kb < NB; ++kb)
+    for (int kb = 0; kb < NB; ++kb) v[kb] = fmax_num(fmax_num(s[kb][0], s[kb][1]), fmax_num(s[kb][2], s[kb][3]));
 #pragma unroll
-        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kb][i]);
-    mx = rg.max(mx) * c;
-    const bool grow = mx > m + kLazy;  // false while both are -inf
-    const bool rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
-    alpha = 1.0f;
-    if (rescale) {
-        const float m_new = fmaxf(m, mx);
-        alpha = fast_exp2(m - (m_new == kNegInf ? 0.0f : m_new));
-        m = m_new;
+    for (int w = NB / 2; w >= 1; w /= 2)
+#pragma unroll
+        for (int kb = 0; kb < w; ++kb) v[kb] = fmax_num(v[kb], v[kb + w]);
+    return v[0];
+}
+template <int NB>
+__device__ __forceinline__ float tree_sum(const f32x4 (&s)[NB]) {
+    float v[NB];
+#pragma unroll
+    for (int kb = 0; kb < NB; ++kb) v[kb] = (s[kb][0] + s[kb][1]) + (s[kb][2] + s[kb][3]);
+#pragma unroll
+    for (int w = NB / 2; w >= 1; w /= 2)
+#pragma unroll
+        for (int kb = 0; kb < w; ++kb) v[kb] = v[kb] + v[kb + w];
+    return v[0];
+}
+
+// Online-softmax update of all RB 16-row blocks a wave owns, each with NB
+// 16-key blocks of raw scores (hidden keys already -inf).  m and l are kept
+// in base-2 units of the scaled scores: c = sm_scale * log2(e) > 0, so
+// max(c s) = c max(s) and every probability is one FMA and one exp2.  The row
+// blocks are processed side by side and reductions are balanced trees, so the
+// dependency chains stay short.
+//
+// The reference max m is refreshed lazily: only when some row of the wave
+// sees its max grow by more than kLazy (or has no reference yet).  Otherwise
+// probabilities are taken against the stale m, so they stay below 2^kLazy, and
+// the rescale of the O accumulators (the most expensive VALU work per tile)
+// is skipped.  The result is exact either way: out = O / l and
+// lse = m + log2(l) use the same reference.  Returns true (wave-uniform) when
+// every O block rb must be multiplied by alpha[rb].  Leaves the probabilities
+// in s.
+template <int RB, int NB>
+__device__ __forceinline__ bool softmax_update(const RowGroup& rg, f32x4 (&s)[RB][NB], float c, float (&m)[RB],
+                                               float (&l)[RB], float (&alpha)[RB]) {
+    float mx[RB];
+    bool grow = false;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) mx[rb] = tree_max<NB>(s[rb]);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        mx[rb] = rg.max(mx[rb]) * c;
+        grow |= mx[rb] > m[rb] + kLazy;  // false while both are -inf
     }
-    const float m_use = m == kNegInf ? 0.0f : m;
-    float sum = 0.0f;
+    const bool rescale = __builtin_amdgcn_ballot_w64(grow) != 0;
+    float m_use[RB];
 #pragma unroll
-    for (int kb = 0; kb < NB; ++kb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float p = fast_exp2(fmaf(s[kb][i], c, -m_use));
-            s[kb][i] = p;
-            sum += p;
+    for (int rb = 0; rb < RB; ++rb) {
+        alpha[rb] = 1.0f;
+        if (rescale) {
+            const float m_new = fmax_num(m[rb], mx[rb]);
+            alpha[rb] = fast_exp2(m[rb] - (m_new == kNegInf ? 0.0f : m_new));
+            m[rb] = m_new;
         }
-    l = rescale ? l * alpha + sum : l + sum;  // per-lane partial; row total reduced at the end
+        m_use[rb] = m[rb] == kNegInf ? 0.0f : m[rb];
+    }
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s[rb][kb][i] = fast_exp2(fmaf(s[rb][kb][i], c, -m_use[rb]));
+    // The sums are taken over the fp32 probabilities, not over their bf16
+    // roundings that enter P.V: a row dominated by a few keys would otherwise
+    // carry up to 2^-9 relative error into lse.
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const float sum = tree_sum<NB>(s[rb]);  // per-lane partial; row total reduced at the end
+        l[rb] = rescale ? l[rb] * alpha[rb] + sum : l[rb] + sum;
+    }
     return rescale;
 }
 
 // ---------------------------------------------------------------------------
-// Multi-row tile kernel: one workgroup = 128 query rows of one query head
-// (4 waves x 2 blocks of 16 rows) against the item's key range, 64 keys per
-// LDS tile, K and V tiles double-buffered in LDS.
+// Multi-row tile kernel: one workgroup = 64 * RBW query rows of one query head
+// (4 waves x RBW blocks of 16 rows) against the item's key range, 64 keys per
+// tile, K and V tiles double-buffered in LDS.
+//
+// K/V tiles go from HBM straight into LDS (buffer loads with the LDS bit: lane
+// i of a wave writes bytes [16 i, 16 i + 16) after the wave's base address), so
+// no VGPRs, no LDS store instructions and no wait for the data sit between a
+// tile's load and its use.  Rows are stored unpadded (2 D bytes) and the
+// 16-byte chunks of each row are XOR-permuted by a function of the row, chosen
+// so that the lanes served together by the K fragment reads (16 rows, one
+// chunk column) and by the transposing V reads (8 rows, 32 bytes each) hit
+// distinct banks.  The permutation is applied on the load side: the lane that
+// fills physical chunk p of row r fetches logical chunk p ^ swz(r).
 // ---------------------------------------------------------------------------
 template <int D>
-__global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
+__device__ __forceinline__ int k_swizzle(int row) {  // 16-byte chunk XOR for K rows
+    return D == 128 ? (row & 15) : ((row >> 1) & 7);
+}
+template <int D>
+__device__ __forceinline__ int v_swizzle(int row) {  // 16-byte chunk XOR for V rows (even: 32-byte pairs stay whole)
+    return D == 128 ? ((row & 7) << 1) : (((row >> 1) & 3) << 1);
+}
+
+// 16-byte direct global -> LDS load of one wave: lane i writes LDS bytes
+// [lds_addr + 16 i, +16).  Issued from assembly so that the compiler does not
+// put a wait for it in front of every LDS read (it cannot tell the tile being
+// read from the tile being filled); the kernel waits itself (dma_barrier)
+// before reading a filled tile.
+__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+                 :
+                 : "v"(voff), "s"(r), "s"(lds_addr)
+                 : "memory", "m0");
+}
+// Waits for this wave's direct loads and LDS reads, then for the workgroup.
+__device__ __forceinline__ void dma_barrier() {
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+typedef __attribute__((address_space(3))) char lds_char;
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+    return (uint32_t)(uintptr_t)(const lds_char*)(p);
+}
+
+template <int D, int RBW>
+__global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
     constexpr int BN = kTileKeys;
-    constexpr int KS = D + 8;   // K row stride in LDS: 16-byte skew per row
-    constexpr int VS = D + 16;  // V row stride in LDS: 32-byte skew per row
-    constexpr int DS = D / 32;  // MFMA steps over the head dimension
-    constexpr int DB = D / 16;  // 16-wide blocks of O^T
-    constexpr int CH = D / 8;   // 16-byte chunks per key row
-    constexpr int LOADS = BN * CH / 256;
-    __shared__ __attribute__((aligned(16))) bf16_t k_lds[2][BN * KS];
-    __shared__ __attribute__((aligned(16))) bf16_t v_lds[2][BN * VS];
+    constexpr int RBY = 2 * D;       // bytes per K/V row in LDS
+    constexpr int CH = D / 8;        // 16-byte chunks per row
+    constexpr int DS = D / 32;       // MFMA steps over the head dimension
+    constexpr int DB = D / 16;       // 16-wide blocks of O^T
+    constexpr int NLD = CH / 4;      // direct loads per wave, matrix and tile
+    constexpr int RPL = 64 / CH;     // rows filled by one wave-wide load
+    constexpr int TB = BN * RBY;     // bytes of one K or V tile
+    __shared__ __attribute__((aligned(1024))) char lds[2][2][TB];  // [buffer][K, V]
 
     const WorkItem it = a.items[blockIdx.x];
     const SeqInfo si = a.seqs[it.seq];
@@ -188,12 +281,12 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
     const RowGroup rg;
 
     // ---- rows owned by this lane ------------------------------------------
-    int32_t lo[2], hi[2];
-    bool valid[2];
-    bf16x8 qf[2][DS];
+    int32_t lo[RBW], hi[RBW];
+    bool valid[RBW];
+    bf16x8 qf[RBW][DS];
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-        const int r = wave * 32 + rb * 16 + n;
+    for (int rb = 0; rb < RBW; ++rb) {
+        const int r = wave * 16 * RBW + rb * 16 + n;
         valid[rb] = r < it.nrows;
         lo[rb] = 0;
         hi[rb] = 0;
@@ -210,8 +303,8 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
         }
     }
     // wave-uniform bounds: intervals never shrink from one row to the next
-    const int wr0 = wave * 32;
-    const int wr1 = min(wave * 32 + 31, it.nrows - 1);
+    const int wr0 = wave * 16 * RBW;
+    const int wr1 = min(wr0 + 16 * RBW - 1, it.nrows - 1);
     const bool wave_active = wr0 < it.nrows;
     int32_t w_lo_min = 0, w_lo_max = 0, w_hi_min = 0, w_hi_max = 0;
     if (wave_active) {
@@ -219,19 +312,44 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
         row_interval(a, si, it, it.row0 + wr1, w_lo_max, w_hi_max);
     }
 
-    float m[2] = {kNegInf, kNegInf}, l[2] = {0.0f, 0.0f};
-    f32x4 o[2][DB];
+    float m[RBW], l[RBW];
+    f32x4 o[RBW][DB];
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+    for (int rb = 0; rb < RBW; ++rb)
 #pragma unroll
         for (int db = 0; db < DB; ++db) o[rb][db] = f32x4{0, 0, 0, 0};
+#pragma unroll
+    for (int rb = 0; rb < RBW; ++rb) {
+        m[rb] = kNegInf;
+        l[rb] = 0.0f;
+    }
 
+    // ---- LDS read offsets (per lane, the same for every tile) ----------------
+    // K fragment (kb, s): row kb*16 + n, logical chunk 4 s + grp.
+    uint32_t koff[DS];
+    {
+        const int sw = k_swizzle<D>(n);
+#pragma unroll
+        for (int s = 0; s < DS; ++s) koff[s] = n * RBY + (((4 * s + grp) ^ sw) << 4);
+    }
+    // V^T fragment (c, db, half h): row 32 c + 16 h + 4 grp + n / 4, bf16
+    // column 16 db + 4 (n & 3), i.e. logical chunk 2 db + (n & 3) / 2.
+    uint32_t voff[DB];
+    {
+        const int vr = 4 * grp + (n >> 2);
+        const int vh = v_swizzle<D>(vr) >> 1;
+        const uint32_t base = vr * RBY + (((n & 3) >> 1) << 4) + ((n & 1) << 3);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) voff[db] = base + ((db ^ vh) << 5);
+    }
+
+    // ---- direct K/V loads ---------------------------------------------------
     // Page indices of 64 consecutive pages (16 tiles) of the item sit in one
     // register per wave (lane i = page i of the window) and are read back with
-    // readlane: the rows a thread loads share a page across the wave, so no
-    // block-table load stands between a tile and its K/V loads.  Loads are
-    // issued unconditionally from in-pool addresses; rows past the item's end
-    // (or on a page outside the pool) are zeroed when stored to LDS.
+    // readlane, so no block-table load stands between a tile and its K/V loads.
+    // Load j of wave w fills rows (4 j + w) RPL .. +RPL of the tile, which lie in
+    // one page; a thread's slot inside that page and its logical chunk are the
+    // same for every tile and every j.
     const int32_t page0 = it.k_begin >> 4;
     const int32_t n_pages = ((it.k_end + 15) >> 4) - page0;
     auto load_pages = [&](int first) {
@@ -244,24 +362,20 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
     const int64_t slot_stride = (int64_t)a.hkv * D;
     const size_t page_bytes = (size_t)16 * slot_stride * sizeof(bf16_t);
-    constexpr int PPT = BN / 16;  // pages per tile
-    // byte offset of each of this thread's rows inside its page: the same for every tile
-    uint32_t toff[LOADS];
-#pragma unroll
-    for (int j = 0; j < LOADS; ++j) {
-        const int c = tid + 256 * j;
-        const int row = c / CH, col = (c % CH) * 8;
-        toff[j] = (uint32_t)((((row & 15) * slot_stride) + (int64_t)kvh * D + col) * sizeof(bf16_t));
-    }
+    const int lrow0 = wave * RPL + lane / CH;  // tile row of load j = 0
+    const int pch = lane % CH;                 // physical chunk this lane fills
+    const uint32_t slot_off = (uint32_t)(((lrow0 & 15) * slot_stride + (int64_t)kvh * D) * sizeof(bf16_t));
+    const uint32_t gk = slot_off + ((pch ^ k_swizzle<D>(lrow0)) << 4);
+    const uint32_t gv = slot_off + ((pch ^ v_swizzle<D>(lrow0)) << 4);
     const char* kbase = reinterpret_cast<const char*>(a.k);
     const char* vbase = reinterpret_cast<const char*>(a.v);
-    uint4 kreg[LOADS], vreg[LOADS];
+    const uint32_t lds0 = lds_address(&lds[0][0][0]);
     // Rows past the item's end read zeros through the buffer range check (their
     // offset is pushed past the page), and a page outside the pool gets an
-    // empty range: no selects on the data and no access outside the pool.
+    // empty range: no access outside the pool, and zeros in LDS.
     constexpr uint32_t kOutOfRange = 0x80000000u;
-    auto load_tile = [&](int tix) {
-        const int rel0 = tix * PPT;
+    auto issue_tile = [&](int tix) {
+        const int rel0 = tix * (BN / 16);
         if ((rel0 >> 6) != win) {  // next window of page indices
             ++win;
             pw_cur = pw_next;
@@ -269,63 +383,52 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
         }
         const int32_t k0 = it.k_begin + tix * BN;
         const bool tail = k0 + BN > it.k_end;
+        const uint32_t lbuf = lds0 + (uint32_t)((tix & 1) * 2 * TB);
 #pragma unroll
-        for (int j = 0; j < LOADS; ++j) {
-            // page of this row within the tile: the same for the whole wave
-            const int pg = (wave_u * 64 / CH) / 16 + (256 / CH / 16) * j;
+        for (int j = 0; j < NLD; ++j) {
+            const int pg = ((4 * j + wave_u) * RPL) >> 4;  // page of this load within the tile
             const int32_t page = __builtin_amdgcn_readlane(pw_cur, (rel0 + pg) & 63);
             const bool ok = (uint32_t)page < (uint32_t)a.num_pages;
             page_err |= !ok && k0 + 16 * pg < it.k_end;
             const size_t pofs = ok ? (size_t)page * page_bytes : 0;
             const uint32_t nrec = ok ? (uint32_t)page_bytes : 0u;
-            uint32_t off = toff[j];
-            if (tail) off = k0 + (tid + 256 * j) / CH < it.k_end ? off : kOutOfRange;
-            kreg[j] = load16_at(page_rsrc(kbase, pofs, nrec), off);
-            vreg[j] = load16_at(page_rsrc(vbase, pofs, nrec), off);
-        }
-    };
-    auto store_tile = [&](int buf) {
-#pragma unroll
-        for (int j = 0; j < LOADS; ++j) {
-            const int c = tid + 256 * j;
-            const int row = c / CH, col = (c % CH) * 8;
-            *reinterpret_cast<uint4*>(&k_lds[buf][row * KS + col]) = kreg[j];
-            *reinterpret_cast<uint4*>(&v_lds[buf][row * VS + col]) = vreg[j];
+            const bool live = !tail || k0 + lrow0 + 4 * j * RPL < it.k_end;
+            const uint32_t dst = lbuf + (uint32_t)((4 * j + wave_u) * 1024);
+            lds_dma16(page_rsrc(kbase, pofs, nrec), live ? gk : kOutOfRange, dst);
+            lds_dma16(page_rsrc(vbase, pofs, nrec), live ? gv : kOutOfRange, dst + TB);
         }
     };
 
     const float c2 = a.scale_log2;
     const int n_tiles = (it.k_end - it.k_begin + BN - 1) / BN;
-    load_tile(0);
-    store_tile(0);
-    load_tile(min(1, n_tiles - 1));
-    lds_barrier();
-
-    // one tile of K/V loads in flight while the previous tile is computed; the
-    // last tiles reload the final tile so the loop body stays uniform
+    issue_tile(0);
     for (int tix = 0; tix < n_tiles; ++tix) {
-        const int32_t k0 = it.k_begin + tix * BN;
-        const int buf = tix & 1;
+        // tile tix has landed for every wave, and every wave is done with tile
+        // tix - 1, whose buffer the next loads overwrite
+        dma_barrier();
+        if (tix + 1 < n_tiles) issue_tile(tix + 1);
 
+        const int32_t k0 = it.k_begin + tix * BN;
+        const char* kl = &lds[tix & 1][0][0];
+        const char* vl = &lds[tix & 1][1][0];
         if (wave_active && k0 < w_hi_max && k0 + BN > w_lo_min) {
             const bool full = k0 >= w_lo_max && k0 + BN <= w_hi_min;
-            f32x4 sc[2][4];
+            f32x4 sc[RBW][4];
 #pragma unroll
             for (int kb = 0; kb < 4; ++kb) {
                 bf16x8 kf[DS];
 #pragma unroll
-                for (int s = 0; s < DS; ++s)
-                    kf[s] = *reinterpret_cast<const bf16x8*>(&k_lds[buf][(kb * 16 + n) * KS + 32 * s + 8 * grp]);
+                for (int s = 0; s < DS; ++s) kf[s] = *reinterpret_cast<const bf16x8*>(kl + kb * 16 * RBY + koff[s]);
 #pragma unroll
-                for (int rb = 0; rb < 2; ++rb) sc[rb][kb] = mfma16(kf[0], qf[rb][0], f32x4{0, 0, 0, 0});
+                for (int rb = 0; rb < RBW; ++rb) sc[rb][kb] = mfma16(kf[0], qf[rb][0], f32x4{0, 0, 0, 0});
 #pragma unroll
                 for (int s = 1; s < DS; ++s)
 #pragma unroll
-                    for (int rb = 0; rb < 2; ++rb) sc[rb][kb] = mfma16(kf[s], qf[rb][s], sc[rb][kb]);
+                    for (int rb = 0; rb < RBW; ++rb) sc[rb][kb] = mfma16(kf[s], qf[rb][s], sc[rb][kb]);
             }
+            if (!full) {
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-                if (!full) {
+                for (int rb = 0; rb < RBW; ++rb) {
                     // key k0 + 4 grp + c is visible iff lo <= key < hi
                     const int32_t lo_r = lo[rb] - (k0 + 4 * grp), hi_r = hi[rb] - (k0 + 4 * grp);
 #pragma unroll
@@ -336,41 +439,40 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
                             if (!(c >= lo_r && c < hi_r)) sc[rb][kb][i] = kNegInf;
                         }
                 }
-                float alpha;
-                if (softmax_update<4>(rg, sc[rb], c2, m[rb], l[rb], alpha)) {
+            }
+            float alpha[RBW];
+            if (softmax_update<RBW, 4>(rg, sc, c2, m, l, alpha)) {
 #pragma unroll
-                    for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
-                }
+                for (int rb = 0; rb < RBW; ++rb)
+#pragma unroll
+                    for (int db = 0; db < DB; ++db) o[rb][db] *= alpha[rb];
             }
 #pragma unroll
             for (int c = 0; c < 2; ++c) {
-                bf16x8 pf[2];
+                bf16x8 pf[RBW];
 #pragma unroll
-                for (int rb = 0; rb < 2; ++rb) pf[rb] = to_bf16x8(sc[rb][2 * c], sc[rb][2 * c + 1]);
+                for (int rb = 0; rb < RBW; ++rb) pf[rb] = to_bf16x8(sc[rb][2 * c], sc[rb][2 * c + 1]);
                 bf16x8 vf[DB];
 #pragma unroll
                 for (int db = 0; db < DB; ++db) {
-                    const bf16_t* base = &v_lds[buf][(32 * c + 4 * grp + (n >> 2)) * VS + db * 16 + (n & 3) * 4];
-                    vf[db] = cat(lds_read_tr16(base), lds_read_tr16(base + 16 * VS));
+                    const bf16_t* base = reinterpret_cast<const bf16_t*>(vl + 32 * c * RBY + voff[db]);
+                    vf[db] = cat(lds_read_tr16(base), lds_read_tr16(base + 16 * D));
                 }
 #pragma unroll
                 for (int db = 0; db < DB; ++db)
 #pragma unroll
-                    for (int rb = 0; rb < 2; ++rb) o[rb][db] = mfma16(vf[db], pf[rb], o[rb][db]);
+                    for (int rb = 0; rb < RBW; ++rb) o[rb][db] = mfma16(vf[db], pf[rb], o[rb][db]);
             }
         }
-        store_tile(buf ^ 1);
-        load_tile(min(tix + 2, n_tiles - 1));
-        lds_barrier();
     }
     if (page_err && lane == 0) atomicOr(a.err, MSTAR_DEVERR_PAGE_RANGE_BIT);
 
     // ---- epilogue -------------------------------------------------------------
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
+    for (int rb = 0; rb < RBW; ++rb) {
         const float lt = rg.sum(l[rb]);
         if (!valid[rb]) continue;
-        const int r = wave * 32 + rb * 16 + n;
+        const int r = wave * 16 * RBW + rb * 16 + n;
         const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
         const float lse = lt > 0.0f ? (m[rb] + __log2f(lt)) * kLn2 : kNegInf;
         if (it.part < 0) {
@@ -561,9 +663,9 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
         asm volatile("" ::: "memory");
 
         const bool full = k0 >= lo_max && k0 + SK <= hi_min;
+        if (!full) {
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-            if (!full) {
+            for (int rb = 0; rb < RB; ++rb) {
                 const int32_t lo_r = lo[rb] - (k0 + 4 * grp), hi_r = hi[rb] - (k0 + 4 * grp);
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb)
@@ -573,11 +675,13 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
                         if (!(c >= lo_r && c < hi_r)) sc[rb][kb][e] = kNegInf;
                     }
             }
-            float alpha;
-            if (softmax_update<2>(rg, sc[rb], a.scale_log2, m[rb], l[rb], alpha)) {
+        }
+        float alpha[RB];
+        if (softmax_update<RB, 2>(rg, sc, a.scale_log2, m, l, alpha)) {
 #pragma unroll
-                for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
-            }
+            for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+                for (int db = 0; db < DB; ++db) o[rb][db] *= alpha[rb];
         }
         bf16x8 pf[RB];
 #pragma unroll
@@ -810,10 +914,9 @@ __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
 
 hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s) {
     if (a.n_items == 0) return hipSuccess;
-    if (head_dim == 64)
-        hipLaunchKernelGGL(tile_kernel<64>, dim3(a.n_items), dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL(tile_kernel<128>, dim3(a.n_items), dim3(256), 0, s, a);
+    const dim3 g(a.n_items), b(256);
+    if (head_dim == 64) hipLaunchKernelGGL((tile_kernel<64, 2>), g, b, 0, s, a);
+    else hipLaunchKernelGGL((tile_kernel<128, 2>), g, b, 0, s, a);
     return hipGetLastError();
 }
 
