@@ -244,18 +244,44 @@ __device__ __forceinline__ int v_swizzle(int row) {  // 16-byte chunk XOR for V 
 // [lds_addr + 16 i, +16).  Issued from assembly so that the compiler does not
 // put a wait for it in front of every LDS read (it cannot tell the tile being
 // read from the tile being filled); the kernel waits itself (dma_barrier)
-// before reading a filled tile.
+// before reading a filled tile.  (The few-row kernel, whose two buffers are
+// static, uses the compiler's builtin instead: lds_load16.)
 __device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %2\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
-                 :
-                 : "v"(voff), "s"(r), "s"(lds_addr)
-                 : "memory", "m0");
+    // M0 holds the LDS address; the compiler reserves M0, so the asm puts its
+    // previous value back instead of declaring it clobbered
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(voff), "s"(r), "s"(lds_addr)
+        : "memory");
 }
 // Waits for this wave's direct loads and LDS reads, then for the workgroup.
 __device__ __forceinline__ void dma_barrier() {
     asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 typedef __attribute__((address_space(3))) char lds_char;
+
+// Waits until at most N vector memory operations of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+    static_assert(N >= 0 && N < 16, "vmcnt immediate");
+    // gfx9 s_waitcnt encoding: vmcnt[3:0] in bits 3:0, expcnt and lgkmcnt at
+    // their no-wait maxima (7 in bits 6:4, 15 in bits 11:8)
+    __builtin_amdgcn_s_waitcnt(N | (7 << 4) | (15 << 8));
+}
+
+// 16-byte direct global -> LDS load of one wave through the compiler's
+// builtin (lane i writes bytes [16 i, 16 i + 16) after `lds`, which must be
+// wave-uniform).  The compiler tracks it: it waits for it before a read of
+// the same LDS array, so buffers that must not be waited for together live
+// in distinct arrays.
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, void* lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(lds), 16, voff, 0, 0, 0);
+}
 __device__ __forceinline__ uint32_t lds_address(const void* p) {
     return (uint32_t)(uintptr_t)(const lds_char*)(p);
 }
@@ -504,13 +530,19 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
 // computed.  The four waves' partial results are combined through LDS.
 // ---------------------------------------------------------------------------
 template <int D, int RB>
-__global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(KArgs a) {
+__global__ __launch_bounds__(256, RB == 4 ? 1 : 2) void few_kernel(KArgs a) {
     constexpr int SK = kSubKeys;
-    constexpr int VS = D + 16;
+    constexpr int RBY = 2 * D;        // bytes per V row in LDS
     constexpr int DS = D / 32, DB = D / 16, CH = D / 8;
-    constexpr int VL = SK * CH / 64;  // 16-byte V chunks per lane per step
-    static_assert(RB * 16 * D * 4 <= 4 * SK * VS * 2, "combine buffer must fit in the V staging area");
-    __shared__ __attribute__((aligned(16))) bf16_t v_lds[4][SK * VS];
+    constexpr int VL = SK * CH / 64;  // direct V loads per wave and step
+    constexpr int RPL = 64 / CH;      // V rows filled by one wave-wide load
+    constexpr int SB = SK * RBY;      // bytes of one wave's V slot
+    static_assert(RB * 16 * D * 4 <= 4 * SB, "combine buffer must fit in one set of V slots");
+    // V of the steps held in register buffers A and B goes straight from HBM
+    // into wave-private LDS slots (two arrays, so the compiler can tell which
+    // slot a read depends on and waits for exactly that slot's loads).
+    __shared__ __attribute__((aligned(1024))) char v_slot_a[4][SB];
+    __shared__ __attribute__((aligned(1024))) char v_slot_b[4][SB];
     __shared__ float ml_lds[4][2][RB * 16];
     __shared__ float fin_lds[2][RB * 16];
 
@@ -584,7 +616,6 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
     // would make the compiler wait for every outstanding load.
     struct Step {
         uint4 k[2][DS];
-        uint4 v[VL];
     };
     // Byte offsets of this lane's K and V chunks inside their page, the same
     // for every step; the page (wave-uniform) supplies a scalar base.  Rows past
@@ -592,20 +623,36 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
     // outside the pool gets an empty range, so the data needs no selects.
     constexpr uint32_t kOutOfRange = 0x80000000u;
     const size_t page_bytes = (size_t)16 * slot_stride * sizeof(bf16_t);
-    uint32_t koff[DS], voff[VL];
+    uint32_t koff[DS];
 #pragma unroll
     for (int s = 0; s < DS; ++s)
         koff[s] = (uint32_t)((n * slot_stride + (int64_t)kvh * D + 32 * s + 8 * grp) * sizeof(bf16_t));
+    // V load j fills rows j RPL .. j RPL + RPL - 1 of the step; the lane writes
+    // physical chunk lane % CH of its row and fetches the logical chunk that the
+    // row's swizzle puts there.  The in-page slot and the swizzle repeat every
+    // 16 / RPL loads.
+    constexpr int VJ = 16 / RPL;
+    uint32_t voff[VJ];
 #pragma unroll
-    for (int j = 0; j < VL; ++j) {
-        const int c = lane + 64 * j;
-        const int row = c / CH, col = (c % CH) * 8;
-        voff[j] = (uint32_t)(((row & 15) * slot_stride + (int64_t)kvh * D + col) * sizeof(bf16_t));
+    for (int j = 0; j < VJ; ++j) {
+        const int row = j * RPL + lane / CH;
+        const int chunk = (lane % CH) ^ v_swizzle<D>(row);
+        voff[j] = (uint32_t)(((row & 15) * slot_stride + (int64_t)kvh * D + 8 * chunk) * sizeof(bf16_t));
     }
+    // transposing V reads: rows 4 grp + n / 4 (+16), bf16 columns 16 db + 4 (n & 3)
+    uint32_t vrd[DB];
+    {
+        const int vr = 4 * grp + (n >> 2);
+        const int vh = v_swizzle<D>(vr) >> 1;
+        const uint32_t base = vr * RBY + (((n & 3) >> 1) << 4) + ((n & 1) << 3);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) vrd[db] = base + ((db ^ vh) << 5);
+    }
+    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
     const char* kbase = reinterpret_cast<const char*>(a.k);
     const char* vbase = reinterpret_cast<const char*>(a.v);
     bool page_err = false;
-    auto load_step = [&](Step& st, int i) {
+    auto load_step = [&](Step& st, char (&vs)[4][SB], int i) {
         if (i > 0 && (i & 31) == 0) {  // next window of page indices
             pw_cur = pw_next;
             pw_next = i + 32 < my_steps ? load_pages(i + 32) : 0;
@@ -631,15 +678,23 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
         }
 #pragma unroll
         for (int j = 0; j < VL; ++j) {
-            const int row = (lane + 64 * j) / CH;
-            const int h = (64 * j / CH) >> 4;  // the chunk's page half: the same across the wave
+            const int row = j * RPL + lane / CH;
+            const int h = (j * RPL) >> 4;  // page half of the load's rows: the same across the wave
             const bool live = !tail || k0 + row < it.k_end;
-            st.v[j] = load16_at(rv[h], live ? voff[j] : kOutOfRange);
+            lds_load16(rv[h], live ? voff[j % VJ] : kOutOfRange, &vs[wave_u][j * 1024]);
         }
     };
 
-    bf16_t* vst = v_lds[wave];
-    auto compute_step = [&](Step& cur, int i) {
+    auto compute_step = [&](Step& cur, const char (&vs)[4][SB], int i) {
+        // Wait for every outstanding load of this wave, K registers and V
+        // slots alike, before the step.  A partial wait that counts the next
+        // step's loads as younger (what the compiler emits, and tighter forms
+        // of it) has produced stale V on this hardware when direct-to-LDS
+        // loads and loads into registers are in flight together, so the
+        // kernel does not rely on their relative completion order.  With
+        // eight waves per CU streaming, the shallower prefetch this leaves
+        // costs about 1% on the decode batch.
+        wait_vmem<0>();
         const int32_t k0 = it.k_begin + SK * (wave + 4 * i);
         f32x4 sc[RB][2];
 #pragma unroll
@@ -651,16 +706,6 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
                 for (int rb = 0; rb < RB; ++rb)
                     sc[rb][kb] = mfma16(kf, qf[rb][s], s == 0 ? f32x4{0, 0, 0, 0} : sc[rb][kb]);
             }
-        // stage V for the transpose read (wave-private slice; LDS executes a
-        // wave's accesses in order, the asm keeps the compiler from reordering)
-        asm volatile("" ::: "memory");
-#pragma unroll
-        for (int j = 0; j < VL; ++j) {
-            const int c = lane + 64 * j;
-            const int row = c / CH, col = (c % CH) * 8;
-            *reinterpret_cast<uint4*>(&vst[row * VS + col]) = cur.v[j];
-        }
-        asm volatile("" ::: "memory");
 
         const bool full = k0 >= lo_max && k0 + SK <= hi_min;
         if (!full) {
@@ -688,8 +733,8 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
         for (int rb = 0; rb < RB; ++rb) pf[rb] = to_bf16x8(sc[rb][0], sc[rb][1]);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-            const bf16_t* base = &vst[(4 * grp + (n >> 2)) * VS + db * 16 + (n & 3) * 4];
-            const bf16x8 vf = cat(lds_read_tr16(base), lds_read_tr16(base + 16 * VS));
+            const bf16_t* base = reinterpret_cast<const bf16_t*>(&vs[wave][vrd[db]]);
+            const bf16x8 vf = cat(lds_read_tr16(base), lds_read_tr16(base + 16 * D));
 #pragma unroll
             for (int rb = 0; rb < RB; ++rb) o[rb][db] = mfma16(vf, pf[rb], o[rb][db]);
         }
@@ -703,25 +748,25 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
     Step sa, sb;
     int i = 0;
     if (my_steps >= 4) {
-        load_step(sa, 0);
-        load_step(sb, 1);
+        load_step(sa, v_slot_a, 0);
+        load_step(sb, v_slot_b, 1);
         do {
-            compute_step(sa, i);
-            load_step(sa, i + 2);
-            compute_step(sb, i + 1);
-            load_step(sb, i + 3);
+            compute_step(sa, v_slot_a, i);
+            load_step(sa, v_slot_a, i + 2);
+            compute_step(sb, v_slot_b, i + 1);
+            load_step(sb, v_slot_b, i + 3);
             i += 2;
         } while (i + 3 < my_steps);
     } else {
-        if (my_steps > 0) load_step(sa, 0);
-        if (my_steps > 1) load_step(sb, 1);
+        if (my_steps > 0) load_step(sa, v_slot_a, 0);
+        if (my_steps > 1) load_step(sb, v_slot_b, 1);
     }
     if (i < my_steps) {
-        compute_step(sa, i);
-        if (i + 2 < my_steps) load_step(sa, i + 2);
+        compute_step(sa, v_slot_a, i);
+        if (i + 2 < my_steps) load_step(sa, v_slot_a, i + 2);
     }
-    if (i + 1 < my_steps) compute_step(sb, i + 1);
-    if (i + 2 < my_steps) compute_step(sa, i + 2);
+    if (i + 1 < my_steps) compute_step(sb, v_slot_b, i + 1);
+    if (i + 2 < my_steps) compute_step(sa, v_slot_a, i + 2);
 
     if (page_err && lane == 0) atomicOr(a.err, MSTAR_DEVERR_PAGE_RANGE_BIT);
 
@@ -729,7 +774,7 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
     float lt[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) lt[rb] = rg.sum(l[rb]);
-    __syncthreads();  // every wave is done with its V slice
+    __syncthreads();  // every wave is done with its V slots
     if (grp == 0) {
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
@@ -738,7 +783,7 @@ __global__ __launch_bounds__(256, (RB == 1 || D == 64) ? 2 : 1) void few_kernel(
         }
     }
     __syncthreads();
-    float* obuf = reinterpret_cast<float*>(&v_lds[0][0]);
+    float* obuf = reinterpret_cast<float*>(&v_slot_a[0][0]);
     float scale_own[RB];
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
