@@ -99,7 +99,7 @@ def cpu_baseline(b, tensors, unit, budget_s=15.0):
     n = int(max(1, min(b.num_seqs, budget_s / max(wall1, 1e-3))))
     wall, cpu, pairs, nbytes = measure(order[:n])
     reps = 1
-    while wall * reps < budget_s * 0.66 and reps < 100:  # a small workload: repeat it
+    while wall < budget_s * 0.66 and reps < 100:  # a small workload: repeat it (wall, cpu are totals)
         w2, c2, _, _ = measure(order[:n])
         wall, cpu, reps = wall + w2, cpu + c2, reps + 1
     wall, cpu = wall / reps, cpu / reps
