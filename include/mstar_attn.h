@@ -196,8 +196,11 @@ int mstar_attn_plan_key_ranges(const mstar_plan_t* plan, int32_t* lo_hi, int32_t
  * items, 2 = fp32 items, 3 = rows merged by the merge kernel) into `items` as
  * int32 records of 8 fields; *count receives the number of records, and at
  * most `capacity` records are written.  For inspection and tests.
- * Work record: seq, head (query head; KV head for class 1), row0, nrows,
- *              key_begin, key_end, partial_slot (-1 = final), -1.
+ * Work record: seq, head (query head; KV head for class 1; -1 for class 0,
+ *              whose records serve every query head), row0, nrows, key_begin,
+ *              key_end, partial_slot (-1 = final), head_stride (class 0 with a
+ *              split key range: query head h, row r writes partial slot
+ *              partial_slot + h * head_stride + r; otherwise -1).
  * Merge record: packed_row, head, slot0, slot_stride, nslots, 0, 0, 0. */
 int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, int32_t* items,
                           int64_t capacity, int64_t* count);

@@ -298,11 +298,20 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
     constexpr int TB = BN * RBY;     // bytes of one K or V tile
     __shared__ __attribute__((aligned(1024))) char lds[2][2][TB];  // [buffer][K, V]
 
-    const WorkItem it = a.items[blockIdx.x];
+    // XCD-aware grid: workgroup i runs on XCD i % 8.  Units (item, KV head)
+    // are dealt to the XCDs in turn and the G query heads of a unit take
+    // consecutive slots on its XCD, so the heads that read the same K/V tiles
+    // share that XCD's L2 and run at about the same time.  The unit count is
+    // padded to a multiple of 8 by the launch; padding workgroups exit.
+    const int xcd = blockIdx.x & 7, slot_on_xcd = blockIdx.x >> 3;
+    const int unit = (slot_on_xcd / a.group) * 8 + xcd;
+    if (unit >= a.n_items * a.hkv) return;
+    const int kvh = unit % a.hkv;
+    const int head = kvh * a.group + slot_on_xcd % a.group;
+    const WorkItem it = a.items[unit / a.hkv];
     const SeqInfo si = a.seqs[it.seq];
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int n = lane & 15, grp = lane >> 4;
-    const int kvh = it.head / a.group;
     const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
     const RowGroup rg;
 
@@ -317,7 +326,7 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
         lo[rb] = 0;
         hi[rb] = 0;
         if (valid[rb]) row_interval(a, si, it, it.row0 + r, lo[rb], hi[rb]);
-        const int64_t qoff = ((int64_t)(si.q_start + it.row0 + r) * a.hq + it.head) * D;
+        const int64_t qoff = ((int64_t)(si.q_start + it.row0 + r) * a.hq + head) * D;
 #pragma unroll
         for (int s = 0; s < DS; ++s) {
             if (valid[rb]) {
@@ -502,7 +511,7 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
         const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
         const float lse = lt > 0.0f ? (m[rb] + __log2f(lt)) * kLn2 : kNegInf;
         if (it.part < 0) {
-            const int64_t row = (int64_t)(si.q_start + it.row0 + r) * a.hq + it.head;
+            const int64_t row = (int64_t)(si.q_start + it.row0 + r) * a.hq + head;
             bf16_t* out = reinterpret_cast<bf16_t*>(a.out) + row * D;
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
@@ -511,7 +520,7 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
             }
             if (grp == 0) a.lse[row] = lse;
         } else {
-            const int64_t slot = it.part + r;
+            const int64_t slot = it.part + (int64_t)head * it.head_stride + r;
             float* po = a.part_o + slot * D;
 #pragma unroll
             for (int db = 0; db < DB; ++db)
@@ -959,7 +968,9 @@ __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
 
 hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s) {
     if (a.n_items == 0) return hipSuccess;
-    const dim3 g(a.n_items), b(256);
+    // (item, KV head) units padded to a multiple of the 8 XCDs, G query heads each
+    const int64_t units = ((int64_t)a.n_items * a.hkv + 7) / 8 * 8;
+    const dim3 g((unsigned)(units * a.group)), b(256);
     if (head_dim == 64) hipLaunchKernelGGL((tile_kernel<64, 2>), g, b, 0, s, a);
     else hipLaunchKernelGGL((tile_kernel<128, 2>), g, b, 0, s, a);
     return hipGetLastError();

@@ -27,9 +27,13 @@ struct SeqInfo {
 //    query row r / G and query head head*G + r % G (G = Hq / Hkv).
 // part < 0: write the final out/lse; otherwise write fp32 partials to slots
 // part + (r - row0), combined afterwards by the merge kernel.
+// One work item.  Few-row and fp32 items name their (KV or query) head;
+// multi-row tile items have head = -1 and serve every query head (the head
+// comes from the launch grid), and for a split tile the partial slot of query
+// head h and row r is part + h * head_stride + r.
 struct WorkItem {
     int32_t seq, head, row0, nrows;
-    int32_t k_begin, k_end, part, unit;  // unit: reserved, -1
+    int32_t k_begin, k_end, part, head_stride;  // head_stride: -1 unless a split tile
 };
 
 // Output (packed_row, head) assembled from nslots partials at

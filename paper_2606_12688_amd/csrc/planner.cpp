@@ -43,6 +43,34 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 struct RowIntervals {
     std::vector<int32_t> lo, hi;
+    std::vector<int64_t> lo_sum, hi_sum;  // prefix sums: lo_sum[i] = lo[0] + ... + lo[i-1]
+
+    void build_sums() {
+        lo_sum.assign(lo.size() + 1, 0);
+        hi_sum.assign(hi.size() + 1, 0);
+        for (size_t i = 0; i < lo.size(); ++i) {
+            lo_sum[i + 1] = lo_sum[i] + lo[i];
+            hi_sum[i + 1] = hi_sum[i] + hi[i];
+        }
+    }
+    // Visible (row, key) pairs of rows [r0, r1) inside keys [kb, ke), i.e. the
+    // sum over rows of max(0, min(hi, ke) - max(lo, kb)).  lo and hi never
+    // decrease from one row to the next and lo < hi, so the rows with a
+    // non-empty overlap are those from the first with hi > kb up to (not
+    // including) the first with lo >= ke, and on that range the min and the
+    // max each switch operand once: O(log rows) with the prefix sums.
+    int64_t pairs(int32_t r0, int32_t r1, int32_t kb, int32_t ke) const {
+        if (r1 <= r0 || ke <= kb) return 0;
+        const auto H0 = hi.begin(), L0 = lo.begin();
+        const int32_t a = (int32_t)(std::upper_bound(H0 + r0, H0 + r1, kb) - H0);  // first hi > kb
+        const int32_t b = (int32_t)(std::lower_bound(L0 + r0, L0 + r1, ke) - L0);  // first lo >= ke
+        if (b <= a) return 0;
+        const int32_t c = (int32_t)(std::lower_bound(H0 + a, H0 + b, ke) - H0);    // first hi >= ke
+        const int32_t d = (int32_t)(std::lower_bound(L0 + a, L0 + b, kb) - L0);    // first lo >= kb
+        const int64_t sum_min_hi = (hi_sum[c] - hi_sum[a]) + (int64_t)ke * (b - c);
+        const int64_t sum_max_lo = (int64_t)kb * (d - a) + (lo_sum[b] - lo_sum[d]);
+        return sum_min_hi - sum_max_lo;
+    }
 };
 
 // Visible interval of every query row of one request.  Returns false (with a
@@ -222,7 +250,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             for (int32_t h = 0; h < P.num_qo_heads; ++h) {
                 for (int32_t row0 = 0; row0 < s.q_len; row0 += kF32Rows) {
                     const int32_t nr = std::min(kF32Rows, s.q_len - row0);
-                    WorkItem w{r, h, row0, nr, align_down16(v.lo[row0]), v.hi[row0 + nr - 1], -1, 0};
+                    WorkItem w{r, h, row0, nr, align_down16(v.lo[row0]), v.hi[row0 + nr - 1], -1, -1};
                     plan.f32.push_back(w);
                 }
             }
@@ -237,12 +265,11 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             }
             plan.decode_rb = std::max<int32_t>(plan.decode_rb, R <= 16 ? 1 : R <= 32 ? 2 : 4);
         } else {
-            for (int32_t h = 0; h < P.num_qo_heads; ++h) {
-                for (int32_t row0 = 0; row0 < s.q_len; row0 += kTileRows) {
-                    const int32_t nr = std::min(kTileRows, s.q_len - row0);
-                    Unit u{r, h, row0, nr, align_down16(v.lo[row0]), v.hi[row0 + nr - 1], 0};
-                    tile_units.push_back(u);
-                }
+            // one unit per row tile, shared by every query head
+            for (int32_t row0 = 0; row0 < s.q_len; row0 += kTileRows) {
+                const int32_t nr = std::min(kTileRows, s.q_len - row0);
+                Unit u{r, -1, row0, nr, align_down16(v.lo[row0]), v.hi[row0 + nr - 1], 0};
+                tile_units.push_back(u);
             }
         }
     }
@@ -267,7 +294,9 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             }
             nch = ceil_div(n, cs);
         }
-        const int32_t G_ = few ? G : 1;
+        // partial slots of a split unit: few-row units [chunk][row]; tile units
+        // [query head][chunk][row]
+        const int64_t heads = few ? 1 : P.num_qo_heads;
         for (int64_t c = 0; c < nch; ++c) {
             WorkItem w;
             w.seq = u.seq;
@@ -277,23 +306,25 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             w.k_begin = (int32_t)(u.k_begin + c * cs);
             w.k_end = (int32_t)std::min<int64_t>(u.k_begin + (c + 1) * cs, u.k_end);
             w.part = nch > 1 ? (int32_t)(slot + c * u.nrows) : -1;
-            w.unit = -1;
+            w.head_stride = (nch > 1 && !few) ? (int32_t)(nch * u.nrows) : -1;
             dst.push_back(w);
         }
         if (nch > 1) {
             const SeqInfo& si = plan.seqs[u.seq];
-            for (int32_t r = 0; r < u.nrows; ++r) {
-                MergeItem m;
-                const int32_t rr = u.row0 + r;
-                m.row = si.q_start + rr / G_;
-                m.head = few ? u.head * G + rr % G : u.head;
-                m.slot0 = (int32_t)(slot + r);
-                m.stride = u.nrows;
-                m.nslots = (int32_t)nch;
-                m.pad0 = m.pad1 = m.pad2 = 0;
-                plan.merges.push_back(m);
+            for (int64_t h = 0; h < heads; ++h) {
+                for (int32_t r = 0; r < u.nrows; ++r) {
+                    MergeItem m;
+                    const int32_t rr = u.row0 + r;
+                    m.row = si.q_start + (few ? rr / G : rr);
+                    m.head = few ? u.head * G + rr % G : (int32_t)h;
+                    m.slot0 = (int32_t)(slot + h * nch * u.nrows + r);
+                    m.stride = u.nrows;
+                    m.nslots = (int32_t)nch;
+                    m.pad0 = m.pad1 = m.pad2 = 0;
+                    plan.merges.push_back(m);
+                }
             }
-            slot += nch * u.nrows;
+            slot += nch * u.nrows * heads;
         }
     };
 
@@ -316,7 +347,8 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         int32_t chunk = 0;
         if (P.flags & MSTAR_FLAG_FORCE_SPLIT) {
             chunk = kTileKeys * 2;
-        } else if (!(P.flags & MSTAR_FLAG_NO_SPLIT) && tile_units.size() < 512 && !tile_units.empty()) {
+        } else if (!(P.flags & MSTAR_FLAG_NO_SPLIT) && (int64_t)tile_units.size() * P.num_qo_heads < 512 &&
+                   !tile_units.empty()) {
             int64_t c = std::max<int64_t>(1024, ceil_div(total, 1024));
             chunk = (int32_t)std::min<int64_t>(ceil_div(c, kTileKeys) * kTileKeys, INT32_MAX / 2);
         }
@@ -326,15 +358,9 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     if (slot > INT32_MAX) { err = "too many partial rows"; return MSTAR_ERR_INVALID_ARG; }
 
     // ---- 5. longest first ------------------------------------------------------
+    for (RowIntervals& v : iv) v.build_sums();
     auto visible_in = [&](const WorkItem& w) -> int64_t {
-        const RowIntervals& v = iv[w.seq];
-        int64_t c = 0;
-        for (int32_t r = 0; r < w.nrows; ++r) {
-            const int32_t i = w.row0 + r;
-            const int32_t a = std::max(v.lo[i], w.k_begin), b = std::min(v.hi[i], w.k_end);
-            if (b > a) c += b - a;
-        }
-        return c;
+        return iv[w.seq].pairs(w.row0, w.row0 + w.nrows, w.k_begin, w.k_end);
     };
     auto lpt = [&](std::vector<WorkItem>& items, bool by_pairs) {
         std::vector<std::pair<int64_t, int32_t>> key(items.size());

@@ -34,18 +34,24 @@ def _coverage(b, flags):
     cover = {}  # (request, query_row, head) -> list of (k_begin, k_end)
     slots = {}
     for kind in (0, 1, 2):
-        for seq, head, row0, nrows, kb, ke, part, _ in pl.items(kind):
+        for seq, head, row0, nrows, kb, ke, part, head_stride in pl.items(kind):
             assert ke > kb
-            for r in range(nrows):
-                rr = row0 + r
-                if kind == 1:
-                    key = (seq, rr // G, head * G + rr % G)
-                else:
-                    key = (seq, rr, head)
-                cover.setdefault(key, []).append((kb, ke))
-                if part >= 0:
-                    assert part + r not in slots
-                    slots[part + r] = key
+            # multi-row tile records serve every query head
+            heads = range(b.num_qo_heads) if kind == 0 else [head]
+            assert (head == -1) == (kind == 0)
+            assert head_stride == -1 or (kind == 0 and part >= 0 and head_stride >= nrows)
+            for h in heads:
+                for r in range(nrows):
+                    rr = row0 + r
+                    if kind == 1:
+                        key = (seq, rr // G, h * G + rr % G)
+                    else:
+                        key = (seq, rr, h)
+                    cover.setdefault(key, []).append((kb, ke))
+                    if part >= 0:
+                        s = part + r + (h * head_stride if kind == 0 else 0)
+                        assert s not in slots
+                        slots[s] = key
     merges = pl.items(3)
     for row, head, slot0, stride, nslots, *_ in merges:
         keys = {slots[slot0 + s * stride] for s in range(nslots)}
