@@ -247,8 +247,8 @@ __device__ __forceinline__ int v_swizzle(int row) {  // 16-byte chunk XOR for V 
 // before reading a filled tile.  (The few-row kernel, whose two buffers are
 // static, uses the compiler's builtin instead: lds_load16.)
 __device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
-    // M0 holds the LDS address; the compiler reserves M0, so the asm puts its
-    // previous value back instead of declaring it clobbered
+    // M0 holds the (wave-uniform) LDS address; the compiler reserves M0, so
+    // the asm puts its previous value back instead of declaring it clobbered
     uint32_t saved;
     asm volatile(
         "s_mov_b32 %0, m0\n\t"
@@ -256,7 +256,20 @@ __device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, uint32_t vof
         "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
         "s_mov_b32 m0, %0"
         : "=&s"(saved)
-        : "v"(voff), "s"(r), "s"(lds_addr)
+        : "v"(voff), "s"(r), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
+        : "memory");
+}
+// 4-byte direct global -> LDS load of one wave: lane i writes LDS bytes
+// [lds_addr + 4 i, +4).  Untracked by the compiler, like lds_dma16.
+__device__ __forceinline__ void lds_dma4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "buffer_load_dword %1, %2, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(voff), "s"(r), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
         : "memory");
 }
 // Waits for this wave's direct loads and LDS reads, then for the workgroup.
@@ -297,6 +310,7 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
     constexpr int RPL = 64 / CH;     // rows filled by one wave-wide load
     constexpr int TB = BN * RBY;     // bytes of one K or V tile
     __shared__ __attribute__((aligned(1024))) char lds[2][2][TB];  // [buffer][K, V]
+    __shared__ __attribute__((aligned(256))) int32_t page_ring[2][64];
 
     // XCD-aware grid: workgroup i runs on XCD i % 8.  Units (item, KV head)
     // are dealt to the XCDs in turn and the G query heads of a unit take
@@ -379,22 +393,35 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
     }
 
     // ---- direct K/V loads ---------------------------------------------------
-    // Page indices of 64 consecutive pages (16 tiles) of the item sit in one
-    // register per wave (lane i = page i of the window) and are read back with
-    // readlane, so no block-table load stands between a tile and its K/V loads.
-    // Load j of wave w fills rows (4 j + w) RPL .. +RPL of the tile, which lie in
-    // one page; a thread's slot inside that page and its logical chunk are the
-    // same for every tile and every j.
+    // The item's page indices pass through a two-window LDS ring (64 pages =
+    // 16 tiles per window).  Wave 0 fills a window with one direct-to-LDS dword
+    // load (lane i writes page 64 w + i at ring[w & 1][i]) a whole window ahead
+    // of its use; like the K/V loads it is covered by the wait at the top of
+    // every tile.  Keeping the page indices out of compiler-tracked registers
+    // matters: a tracked load in the loop makes the compiler wait for every
+    // outstanding load (the just-issued K/V prefetch included) before its
+    // result is first moved.  Load j of wave w fills rows (4 j + w) RPL .. +RPL
+    // of the tile, which lie in one page; a thread's slot inside that page and
+    // its logical chunk are the same for every tile and every j.
     const int32_t page0 = it.k_begin >> 4;
     const int32_t n_pages = ((it.k_end + 15) >> 4) - page0;
-    auto load_pages = [&](int first) {
-        const int pg = first + lane;
-        return pg < n_pages ? bt_row[page0 + pg] : 0;
-    };
-    int32_t pw_cur = load_pages(0), pw_next = n_pages > 64 ? load_pages(64) : 0;
-    int win = 0;
-    bool page_err = false;
     const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int32_t* bt_item = bt_row + page0;
+    // window w of the item's pages: zeros past the last page (range check)
+    auto load_window = [&](int w) {
+        if (wave_u == 0 && 64 * w < n_pages) {
+            // the pointer and size are wave-uniform; readfirstlane puts them in
+            // scalar registers, where a buffer resource must live
+            const uint64_t base = reinterpret_cast<uint64_t>(bt_item);
+            const uint32_t lo32 = __builtin_amdgcn_readfirstlane((uint32_t)base);
+            const uint32_t hi32 = __builtin_amdgcn_readfirstlane((uint32_t)(base >> 32));
+            const __amdgpu_buffer_rsrc_t r =
+                page_rsrc(reinterpret_cast<const char*>(((uint64_t)hi32 << 32) | lo32), 0,
+                          (uint32_t)__builtin_amdgcn_readfirstlane(n_pages * 4));
+            lds_dma4(r, (uint32_t)(64 * w + lane) * 4u, lds_address(&page_ring[w & 1][0]));
+        }
+    };
+    bool page_err = false;
     const int64_t slot_stride = (int64_t)a.hkv * D;
     const size_t page_bytes = (size_t)16 * slot_stride * sizeof(bf16_t);
     const int lrow0 = wave * RPL + lane / CH;  // tile row of load j = 0
@@ -409,20 +436,20 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
     // offset is pushed past the page), and a page outside the pool gets an
     // empty range: no access outside the pool, and zeros in LDS.
     constexpr uint32_t kOutOfRange = 0x80000000u;
+    constexpr int PPT = BN / 16;  // pages per tile
     auto issue_tile = [&](int tix) {
-        const int rel0 = tix * (BN / 16);
-        if ((rel0 >> 6) != win) {  // next window of page indices
-            ++win;
-            pw_cur = pw_next;
-            pw_next = 64 * (win + 1) < n_pages ? load_pages(64 * (win + 1)) : 0;
-        }
+        const int rel0 = tix * PPT;
+        // first tile of window w >= 1: every wave is past its last read of
+        // window w - 1, so its ring slot can take window w + 1
+        if (tix > 0 && (rel0 & 63) == 0) load_window((rel0 >> 6) + 1);
+        const int32_t* ring = &page_ring[(rel0 >> 6) & 1][0];
         const int32_t k0 = it.k_begin + tix * BN;
         const bool tail = k0 + BN > it.k_end;
         const uint32_t lbuf = lds0 + (uint32_t)((tix & 1) * 2 * TB);
 #pragma unroll
         for (int j = 0; j < NLD; ++j) {
             const int pg = ((4 * j + wave_u) * RPL) >> 4;  // page of this load within the tile
-            const int32_t page = __builtin_amdgcn_readlane(pw_cur, (rel0 + pg) & 63);
+            const int32_t page = __builtin_amdgcn_readfirstlane(ring[(rel0 + pg) & 63]);
             const bool ok = (uint32_t)page < (uint32_t)a.num_pages;
             page_err |= !ok && k0 + 16 * pg < it.k_end;
             const size_t pofs = ok ? (size_t)page * page_bytes : 0;
@@ -436,6 +463,16 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
 
     const float c2 = a.scale_log2;
     const int n_tiles = (it.k_end - it.k_begin + BN - 1) / BN;
+    load_window(0);
+    load_window(1);
+    // The Q fragments are consumed here, so the compiler's wait for their loads
+    // sits before any K/V load is in flight (inside the loop it would also
+    // wait for the prefetch).
+#pragma unroll
+    for (int rb = 0; rb < RBW; ++rb)
+#pragma unroll
+        for (int s = 0; s < DS; ++s) asm volatile("" ::"v"(qf[rb][s]));
+    dma_barrier();  // windows 0 and 1 of the page ring have landed
     issue_tile(0);
     for (int tix = 0; tix < n_tiles; ++tix) {
         // tile tix has landed for every wave, and every wave is done with tile
