@@ -295,12 +295,24 @@ __device__ __forceinline__ void wait_vmem() {
 __device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, void* lds) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(lds), 16, voff, 0, 0, 0);
 }
+// The same with a wave-uniform scalar byte offset added to the global address.
+__device__ __forceinline__ void lds_load16s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, void* lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(lds), 16, voff,
+                                             (int)soff, 0, 0);
+}
 __device__ __forceinline__ uint32_t lds_address(const void* p) {
     return (uint32_t)(uintptr_t)(const lds_char*)(p);
 }
 
-template <int D, int RBW>
-__global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
+// K/V of a pool that fits in 2 GB are read through one buffer resource per
+// pool with the page's byte offset in the instruction's scalar offset, so a
+// load costs no scalar work beyond one multiply per page.  Larger pools get a
+// resource per page (SMALL = false).  The 2 GB resource range keeps every
+// valid offset in range and pushes the marker offset below out of range.
+constexpr uint32_t kSmallPoolBytes = 0x80000000u;
+
+template <int D, int RBW, bool SMALL>
+__global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
     constexpr int BN = kTileKeys;
     constexpr int RBY = 2 * D;       // bytes per K/V row in LDS
     constexpr int CH = D / 8;        // 16-byte chunks per row
@@ -309,7 +321,12 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
     constexpr int NLD = CH / 4;      // direct loads per wave, matrix and tile
     constexpr int RPL = 64 / CH;     // rows filled by one wave-wide load
     constexpr int TB = BN * RBY;     // bytes of one K or V tile
-    __shared__ __attribute__((aligned(1024))) char lds[2][2][TB];  // [buffer][K, V]
+    constexpr int PPT = BN / 16;     // pages per tile
+    // the two tile buffers are distinct arrays, so that the compiler, which
+    // tracks the direct loads, waits before a read only for the loads into
+    // the buffer being read
+    __shared__ __attribute__((aligned(1024))) char buf0[2][TB];  // [K, V] of even tiles
+    __shared__ __attribute__((aligned(1024))) char buf1[2][TB];  // [K, V] of odd tiles
     __shared__ __attribute__((aligned(256))) int32_t page_ring[2][64];
 
     // XCD-aware grid: workgroup i runs on XCD i % 8.  Units (item, KV head)
@@ -324,7 +341,9 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
     const int head = kvh * a.group + slot_on_xcd % a.group;
     const WorkItem it = a.items[unit / a.hkv];
     const SeqInfo si = a.seqs[it.seq];
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    // the wave index is wave-uniform; readfirstlane lets the compiler keep
+    // everything derived from it (row bounds, loop decisions) in scalars
+    const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3, lane = tid & 63;
     const int n = lane & 15, grp = lane >> 4;
     const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
     const RowGroup rg;
@@ -405,11 +424,10 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
     // its logical chunk are the same for every tile and every j.
     const int32_t page0 = it.k_begin >> 4;
     const int32_t n_pages = ((it.k_end + 15) >> 4) - page0;
-    const int wave_u = __builtin_amdgcn_readfirstlane(wave);
     const int32_t* bt_item = bt_row + page0;
     // window w of the item's pages: zeros past the last page (range check)
     auto load_window = [&](int w) {
-        if (wave_u == 0 && 64 * w < n_pages) {
+        if (wave == 0 && 64 * w < n_pages) {
             // the pointer and size are wave-uniform; readfirstlane puts them in
             // scalar registers, where a buffer resource must live
             const uint64_t base = reinterpret_cast<uint64_t>(bt_item);
@@ -423,7 +441,7 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
     };
     bool page_err = false;
     const int64_t slot_stride = (int64_t)a.hkv * D;
-    const size_t page_bytes = (size_t)16 * slot_stride * sizeof(bf16_t);
+    const uint32_t page_bytes = (uint32_t)(16 * slot_stride * sizeof(bf16_t));
     const int lrow0 = wave * RPL + lane / CH;  // tile row of load j = 0
     const int pch = lane % CH;                 // physical chunk this lane fills
     const uint32_t slot_off = (uint32_t)(((lrow0 & 15) * slot_stride + (int64_t)kvh * D) * sizeof(bf16_t));
@@ -431,109 +449,146 @@ __global__ __launch_bounds__(256, RBW <= 2 ? 2 : 1) void tile_kernel(KArgs a) {
     const uint32_t gv = slot_off + ((pch ^ v_swizzle<D>(lrow0)) << 4);
     const char* kbase = reinterpret_cast<const char*>(a.k);
     const char* vbase = reinterpret_cast<const char*>(a.v);
-    const uint32_t lds0 = lds_address(&lds[0][0][0]);
+    const __amdgpu_buffer_rsrc_t kpool = page_rsrc(kbase, 0, kSmallPoolBytes);
+    const __amdgpu_buffer_rsrc_t vpool = page_rsrc(vbase, 0, kSmallPoolBytes);
     // Rows past the item's end read zeros through the buffer range check (their
-    // offset is pushed past the page), and a page outside the pool gets an
-    // empty range: no access outside the pool, and zeros in LDS.
+    // offset is pushed out of range), and so does every row of a page outside
+    // the pool: no access outside the pool, and zeros in LDS.
     constexpr uint32_t kOutOfRange = 0x80000000u;
-    constexpr int PPT = BN / 16;  // pages per tile
-    auto issue_tile = [&](int tix) {
+    // Loads of tile tix into buffer `dst` ([K, V]).
+    auto issue_tile = [&](int tix, char (&dst)[2][TB]) {
         const int rel0 = tix * PPT;
         // first tile of window w >= 1: every wave is past its last read of
         // window w - 1, so its ring slot can take window w + 1
         if (tix > 0 && (rel0 & 63) == 0) load_window((rel0 >> 6) + 1);
-        const int32_t* ring = &page_ring[(rel0 >> 6) & 1][0];
-        const int32_t k0 = it.k_begin + tix * BN;
-        const bool tail = k0 + BN > it.k_end;
-        const uint32_t lbuf = lds0 + (uint32_t)((tix & 1) * 2 * TB);
+        // the tile's PPT page indices, one 16-byte LDS read
+        const int4 pq = *reinterpret_cast<const int4*>(&page_ring[(rel0 >> 6) & 1][rel0 & 63]);
+        const int32_t pgs[4] = {pq.x, pq.y, pq.z, pq.w};
+        uint32_t page[NLD];
+        bool all_ok = true;
 #pragma unroll
         for (int j = 0; j < NLD; ++j) {
-            const int pg = ((4 * j + wave_u) * RPL) >> 4;  // page of this load within the tile
-            const int32_t page = __builtin_amdgcn_readfirstlane(ring[(rel0 + pg) & 63]);
-            const bool ok = (uint32_t)page < (uint32_t)a.num_pages;
-            page_err |= !ok && k0 + 16 * pg < it.k_end;
-            const size_t pofs = ok ? (size_t)page * page_bytes : 0;
-            const uint32_t nrec = ok ? (uint32_t)page_bytes : 0u;
-            const bool live = !tail || k0 + lrow0 + 4 * j * RPL < it.k_end;
-            const uint32_t dst = lbuf + (uint32_t)((4 * j + wave_u) * 1024);
-            lds_dma16(page_rsrc(kbase, pofs, nrec), live ? gk : kOutOfRange, dst);
-            lds_dma16(page_rsrc(vbase, pofs, nrec), live ? gv : kOutOfRange, dst + TB);
+            // page of load j within the tile: (4 j + wave) RPL / 16, split so
+            // that the compiler sees a constant for RPL = 4
+            page[j] = (uint32_t)__builtin_amdgcn_readfirstlane(pgs[(j * RPL) / 4 + (wave * RPL) / 16]);
+            all_ok &= page[j] < (uint32_t)a.num_pages;
+        }
+        const int32_t k0 = it.k_begin + tix * BN;
+        const bool tail = k0 + BN > it.k_end;
+        if (SMALL && all_ok && !tail) {
+            // common case: only the page offsets change from tile to tile
+#pragma unroll
+            for (int j = 0; j < NLD; ++j) {
+                const uint32_t soff = page[j] * page_bytes;
+                lds_load16s(kpool, gk, soff, &dst[0][(4 * j + wave) * 1024]);
+                lds_load16s(vpool, gv, soff, &dst[1][(4 * j + wave) * 1024]);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < NLD; ++j) {
+                const int pg = ((4 * j + wave) * RPL) >> 4;  // page of this load within the tile
+                const bool ok = page[j] < (uint32_t)a.num_pages;
+                page_err |= !ok && k0 + 16 * pg < it.k_end;
+                const bool live = ok && (!tail || k0 + lrow0 + 4 * j * RPL < it.k_end);
+                if (SMALL) {
+                    const uint32_t soff = ok ? page[j] * page_bytes : 0u;
+                    lds_load16s(kpool, live ? gk : kOutOfRange, soff, &dst[0][(4 * j + wave) * 1024]);
+                    lds_load16s(vpool, live ? gv : kOutOfRange, soff, &dst[1][(4 * j + wave) * 1024]);
+                } else {
+                    const size_t pofs = ok ? (size_t)page[j] * page_bytes : 0;
+                    const uint32_t nrec = ok ? page_bytes : 0u;
+                    lds_load16s(page_rsrc(kbase, pofs, nrec), live ? gk : kOutOfRange, 0u,
+                                &dst[0][(4 * j + wave) * 1024]);
+                    lds_load16s(page_rsrc(vbase, pofs, nrec), live ? gv : kOutOfRange, 0u,
+                                &dst[1][(4 * j + wave) * 1024]);
+                }
+            }
         }
     };
 
+    // ---- one tile: scores, mask, online softmax, weighted values ---------------
     const float c2 = a.scale_log2;
-    const int n_tiles = (it.k_end - it.k_begin + BN - 1) / BN;
-    load_window(0);
-    load_window(1);
-    // The Q fragments are consumed here, so the compiler's wait for their loads
-    // sits before any K/V load is in flight (inside the loop it would also
-    // wait for the prefetch).
-#pragma unroll
-    for (int rb = 0; rb < RBW; ++rb)
-#pragma unroll
-        for (int s = 0; s < DS; ++s) asm volatile("" ::"v"(qf[rb][s]));
-    dma_barrier();  // windows 0 and 1 of the page ring have landed
-    issue_tile(0);
-    for (int tix = 0; tix < n_tiles; ++tix) {
-        // tile tix has landed for every wave, and every wave is done with tile
-        // tix - 1, whose buffer the next loads overwrite
-        dma_barrier();
-        if (tix + 1 < n_tiles) issue_tile(tix + 1);
-
+    auto compute_tile = [&](int tix, const char (&cur)[2][TB]) {
         const int32_t k0 = it.k_begin + tix * BN;
-        const char* kl = &lds[tix & 1][0][0];
-        const char* vl = &lds[tix & 1][1][0];
-        if (wave_active && k0 < w_hi_max && k0 + BN > w_lo_min) {
-            const bool full = k0 >= w_lo_max && k0 + BN <= w_hi_min;
-            f32x4 sc[RBW][4];
+        if (!(wave_active && k0 < w_hi_max && k0 + BN > w_lo_min)) return;
+        const char* kl = &cur[0][0];
+        const char* vl = &cur[1][0];
+        const bool full = k0 >= w_lo_max && k0 + BN <= w_hi_min;
+        f32x4 sc[RBW][4];
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb) {
-                bf16x8 kf[DS];
+        for (int kb = 0; kb < 4; ++kb) {
+            bf16x8 kf[DS];
 #pragma unroll
-                for (int s = 0; s < DS; ++s) kf[s] = *reinterpret_cast<const bf16x8*>(kl + kb * 16 * RBY + koff[s]);
+            for (int s = 0; s < DS; ++s) kf[s] = *reinterpret_cast<const bf16x8*>(kl + kb * 16 * RBY + koff[s]);
 #pragma unroll
-                for (int rb = 0; rb < RBW; ++rb) sc[rb][kb] = mfma16(kf[0], qf[rb][0], f32x4{0, 0, 0, 0});
+            for (int rb = 0; rb < RBW; ++rb) sc[rb][kb] = mfma16(kf[0], qf[rb][0], f32x4{0, 0, 0, 0});
 #pragma unroll
-                for (int s = 1; s < DS; ++s)
+            for (int s = 1; s < DS; ++s)
 #pragma unroll
-                    for (int rb = 0; rb < RBW; ++rb) sc[rb][kb] = mfma16(kf[s], qf[rb][s], sc[rb][kb]);
+                for (int rb = 0; rb < RBW; ++rb) sc[rb][kb] = mfma16(kf[s], qf[rb][s], sc[rb][kb]);
+        }
+        if (!full) {
+#pragma unroll
+            for (int rb = 0; rb < RBW; ++rb) {
+                // key k0 + 4 grp + c is visible iff lo <= key < hi
+                const int32_t lo_r = lo[rb] - (k0 + 4 * grp), hi_r = hi[rb] - (k0 + 4 * grp);
+#pragma unroll
+                for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int c = kb * 16 + i;
+                        if (!(c >= lo_r && c < hi_r)) sc[rb][kb][i] = kNegInf;
+                    }
             }
-            if (!full) {
+        }
+        float alpha[RBW];
+        if (softmax_update<RBW, 4>(rg, sc, c2, m, l, alpha)) {
 #pragma unroll
-                for (int rb = 0; rb < RBW; ++rb) {
-                    // key k0 + 4 grp + c is visible iff lo <= key < hi
-                    const int32_t lo_r = lo[rb] - (k0 + 4 * grp), hi_r = hi[rb] - (k0 + 4 * grp);
+            for (int rb = 0; rb < RBW; ++rb)
 #pragma unroll
-                    for (int kb = 0; kb < 4; ++kb)
+                for (int db = 0; db < DB; ++db) o[rb][db] *= alpha[rb];
+        }
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const int c = kb * 16 + i;
-                            if (!(c >= lo_r && c < hi_r)) sc[rb][kb][i] = kNegInf;
-                        }
-                }
-            }
-            float alpha[RBW];
-            if (softmax_update<RBW, 4>(rg, sc, c2, m, l, alpha)) {
+        for (int c = 0; c < 2; ++c) {
+            bf16x8 pf[RBW];
 #pragma unroll
-                for (int rb = 0; rb < RBW; ++rb)
+            for (int rb = 0; rb < RBW; ++rb) pf[rb] = to_bf16x8(sc[rb][2 * c], sc[rb][2 * c + 1]);
+            bf16x8 vf[DB];
 #pragma unroll
-                    for (int db = 0; db < DB; ++db) o[rb][db] *= alpha[rb];
+            for (int db = 0; db < DB; ++db) {
+                const bf16_t* base = reinterpret_cast<const bf16_t*>(vl + 32 * c * RBY + voff[db]);
+                vf[db] = cat(lds_read_tr16(base), lds_read_tr16(base + 16 * D));
             }
 #pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                bf16x8 pf[RBW];
+            for (int db = 0; db < DB; ++db)
 #pragma unroll
-                for (int rb = 0; rb < RBW; ++rb) pf[rb] = to_bf16x8(sc[rb][2 * c], sc[rb][2 * c + 1]);
-                bf16x8 vf[DB];
+                for (int rb = 0; rb < RBW; ++rb) o[rb][db] = mfma16(vf[db], pf[rb], o[rb][db]);
+        }
+    };
+
+    const int n_tiles = (it.k_end - it.k_begin + BN - 1) / BN;
+    if (n_tiles > 0) {
+        load_window(0);
+        load_window(1);
+        // The Q fragments are consumed here, so the compiler's wait for their
+        // loads sits before any K/V load is in flight.
 #pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    const bf16_t* base = reinterpret_cast<const bf16_t*>(vl + 32 * c * RBY + voff[db]);
-                    vf[db] = cat(lds_read_tr16(base), lds_read_tr16(base + 16 * D));
-                }
+        for (int rb = 0; rb < RBW; ++rb)
 #pragma unroll
-                for (int db = 0; db < DB; ++db)
-#pragma unroll
-                    for (int rb = 0; rb < RBW; ++rb) o[rb][db] = mfma16(vf[db], pf[rb], o[rb][db]);
+            for (int s = 0; s < DS; ++s) asm volatile("" ::"v"(qf[rb][s]));
+        dma_barrier();  // windows 0 and 1 of the page ring have landed
+        issue_tile(0, buf0);
+        // Tile tix is in buf[tix & 1].  At the top of each tile every wave has
+        // its own loads of the tile done (vmcnt) and every wave is done with
+        // the other buffer (barrier), which the next tile's loads then take.
+        for (int tix = 0; tix < n_tiles; tix += 2) {
+            dma_barrier();
+            if (tix + 1 < n_tiles) issue_tile(tix + 1, buf1);
+            compute_tile(tix, buf0);
+            if (tix + 1 < n_tiles) {
+                dma_barrier();
+                if (tix + 2 < n_tiles) issue_tile(tix + 2, buf0);
+                compute_tile(tix + 1, buf1);
             }
         }
     }
@@ -1008,8 +1063,16 @@ hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s) {
     // (item, KV head) units padded to a multiple of the 8 XCDs, G query heads each
     const int64_t units = ((int64_t)a.n_items * a.hkv + 7) / 8 * 8;
     const dim3 g((unsigned)(units * a.group)), b(256);
-    if (head_dim == 64) hipLaunchKernelGGL((tile_kernel<64, 2>), g, b, 0, s, a);
-    else hipLaunchKernelGGL((tile_kernel<128, 2>), g, b, 0, s, a);
+    // both pools within the range of one buffer resource
+    const uint64_t pool_bytes = (uint64_t)a.num_pages * 16 * a.hkv * head_dim * 2;
+    const bool small = pool_bytes <= kSmallPoolBytes;
+    if (head_dim == 64) {
+        if (small) hipLaunchKernelGGL((tile_kernel<64, 2, true>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((tile_kernel<64, 2, false>), g, b, 0, s, a);
+    } else {
+        if (small) hipLaunchKernelGGL((tile_kernel<128, 2, true>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((tile_kernel<128, 2, false>), g, b, 0, s, a);
+    }
     return hipGetLastError();
 }
 
