@@ -205,6 +205,13 @@ int mstar_attn_plan_key_ranges(const mstar_plan_t* plan, int32_t* lo_hi, int32_t
 int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, int32_t* items,
                           int64_t capacity, int64_t* count);
 
+/* Launch order of the multi-row kernel: *count receives the number of
+ * workgroups (a multiple of 8) and at most `capacity` (tile item, query head)
+ * int32 pairs are written to pairs[2*capacity]; (-1, -1) marks a padding
+ * workgroup.  Workgroup b runs on XCD b % 8; all workgroups that read one
+ * request's pages for one KV head share an XCD.  For inspection and tests. */
+int mstar_attn_plan_tile_order(const mstar_plan_t* plan, int32_t* pairs, int64_t capacity, int64_t* count);
+
 /* Release the plan (host and device memory).  The caller guarantees no
  * enqueued fwd still uses it.  NULL is ignored. */
 void mstar_attn_plan_destroy(mstar_plan_t* plan);

@@ -41,6 +41,7 @@ EXPORTS = [
     "mstar_attn_plan_stats",
     "mstar_attn_plan_key_ranges",
     "mstar_attn_plan_items",
+    "mstar_attn_plan_tile_order",
     "mstar_attn_plan_destroy",
     "mstar_last_error",
 ]
@@ -108,6 +109,8 @@ def lib() -> ctypes.CDLL:
     L.mstar_attn_plan_key_ranges.restype = ctypes.c_int
     L.mstar_attn_plan_items.argtypes = [vp, i32, vp, i64, ctypes.POINTER(i64)]
     L.mstar_attn_plan_items.restype = ctypes.c_int
+    L.mstar_attn_plan_tile_order.argtypes = [vp, vp, i64, ctypes.POINTER(i64)]
+    L.mstar_attn_plan_tile_order.restype = ctypes.c_int
     L.mstar_attn_plan_destroy.argtypes = [vp]
     L.mstar_attn_plan_destroy.restype = None
     L.mstar_last_error.argtypes = []
@@ -182,6 +185,15 @@ class Plan:
         out = np.zeros((max(cnt.value, 1), 8), dtype=np.int32)
         _check_rc(lib().mstar_attn_plan_items(self.handle, kind, out.ctypes.data, cnt.value, ctypes.byref(cnt)))
         return out[: cnt.value]
+
+    def tile_order(self) -> np.ndarray:
+        """(tile item, query head) of every multi-row workgroup in launch order, as an int32 [n, 2] array
+        (``mstar_attn_plan_tile_order``); (-1, -1) marks padding."""
+        cnt = ctypes.c_int64(0)
+        _check_rc(lib().mstar_attn_plan_tile_order(self.handle, None, 0, ctypes.byref(cnt)))
+        out = np.zeros((cnt.value, 2), dtype=np.int32)
+        _check_rc(lib().mstar_attn_plan_tile_order(self.handle, out.ctypes.data, cnt.value, ctypes.byref(cnt)))
+        return out
 
     def destroy(self):
         if self._h:

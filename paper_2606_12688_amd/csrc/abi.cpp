@@ -20,7 +20,7 @@ struct mstar_plan {
     void* dev = nullptr;     // device copy of the plan blob
     void* pinned = nullptr;  // pinned staging copy (kept until destroy)
     size_t bytes = 0;
-    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_err = 0;
+    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_order = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_err = 0;
     double plan_us = 0.0;
 };
 
@@ -80,11 +80,12 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     }
     const mstar::HostPlan& h = plan->host;
 
-    // blob layout: seqs | row_hi | tiles | few | f32 | merges | error word
+    // blob layout: seqs | row_hi | tiles | tile order | few | f32 | merges | error word
     size_t off = 0;
     plan->off_seqs = off;   off = align256(off + h.seqs.size() * sizeof(mstar::SeqInfo));
     plan->off_row_hi = off; off = align256(off + h.row_hi.size() * sizeof(int32_t));
     plan->off_tiles = off;  off = align256(off + h.tiles.size() * sizeof(mstar::WorkItem));
+    plan->off_order = off;  off = align256(off + h.tile_order.size() * sizeof(int32_t));
     plan->off_few = off;    off = align256(off + h.few.size() * sizeof(mstar::WorkItem));
     plan->off_f32 = off;    off = align256(off + h.f32.size() * sizeof(mstar::WorkItem));
     plan->off_merge = off;  off = align256(off + h.merges.size() * sizeof(mstar::MergeItem));
@@ -102,6 +103,7 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
         put(blob, plan->off_seqs, h.seqs);
         put(blob, plan->off_row_hi, h.row_hi);
         put(blob, plan->off_tiles, h.tiles);
+        put(blob, plan->off_order, h.tile_order);
         put(blob, plan->off_few, h.few);
         put(blob, plan->off_f32, h.f32);
         put(blob, plan->off_merge, h.merges);
@@ -192,6 +194,8 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
     if (!h.tiles.empty()) {
         a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_tiles);
         a.n_items = (int32_t)h.tiles.size();
+        a.order = reinterpret_cast<const int32_t*>(blob + plan->off_order);
+        a.n_wgs = (int32_t)(h.tile_order.size() / 2);
         MSTAR_MARK(events_before, 0);
         if ((e = mstar::launch_tiles(a, D, s)) != hipSuccess) return hip_fail(e, "tile kernel launch");
         MSTAR_MARK(events_after, 0);
@@ -290,6 +294,17 @@ MSTAR_EXPORT int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, i
     if (capacity > 0 && !items) return fail(MSTAR_ERR_INVALID_ARG, "items is NULL");
     const size_t m = capacity < 0 ? 0 : std::min<size_t>(n, (size_t)capacity);
     if (m) std::memcpy(items, src, m * 32);
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_attn_plan_tile_order(const mstar_plan_t* plan, int32_t* pairs, int64_t capacity,
+                                            int64_t* count) {
+    if (!plan || !count) return fail(MSTAR_ERR_INVALID_ARG, "plan or count is NULL");
+    const std::vector<int32_t>& o = plan->host.tile_order;
+    *count = (int64_t)(o.size() / 2);
+    if (capacity > 0 && !pairs) return fail(MSTAR_ERR_INVALID_ARG, "pairs is NULL");
+    const size_t m = capacity < 0 ? 0 : std::min<size_t>(o.size() / 2, (size_t)capacity);
+    if (m) std::memcpy(pairs, o.data(), m * 2 * sizeof(int32_t));
     return MSTAR_OK;
 }
 

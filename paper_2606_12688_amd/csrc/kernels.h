@@ -11,6 +11,7 @@ struct KArgs {
     const SeqInfo* seqs;
     const int32_t* row_hi;
     const WorkItem* items;
+    const int32_t* order;  // multi-row launch: (item, query head) per workgroup
     const void* q;
     const void* k;
     const void* v;
@@ -21,6 +22,7 @@ struct KArgs {
     float* part_lse;  // [partial_slots] fp32 natural log
     int32_t* err;     // sticky device error word
     int32_t n_items;
+    int32_t n_wgs;         // multi-row launch: workgroups (a multiple of 8)
     int32_t hq, hkv, group, bt_stride, num_pages;
     float sm_scale;
     float scale_log2;  // sm_scale * log2(e)

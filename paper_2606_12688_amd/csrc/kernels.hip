@@ -329,17 +329,13 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
     __shared__ __attribute__((aligned(1024))) char buf1[2][TB];  // [K, V] of odd tiles
     __shared__ __attribute__((aligned(256))) int32_t page_ring[2][64];
 
-    // XCD-aware grid: workgroup i runs on XCD i % 8.  Units (item, KV head)
-    // are dealt to the XCDs in turn and the G query heads of a unit take
-    // consecutive slots on its XCD, so the heads that read the same K/V tiles
-    // share that XCD's L2 and run at about the same time.  The unit count is
-    // padded to a multiple of 8 by the launch; padding workgroups exit.
-    const int xcd = blockIdx.x & 7, slot_on_xcd = blockIdx.x >> 3;
-    const int unit = (slot_on_xcd / a.group) * 8 + xcd;
-    if (unit >= a.n_items * a.hkv) return;
-    const int kvh = unit % a.hkv;
-    const int head = kvh * a.group + slot_on_xcd % a.group;
-    const WorkItem it = a.items[unit / a.hkv];
+    // The planner's launch order names the (item, query head) of every
+    // workgroup; it keeps the workgroups that read the same K/V pages on one
+    // XCD.  Padding entries (item < 0) exit.
+    const int item = a.order[2 * blockIdx.x], head = a.order[2 * blockIdx.x + 1];
+    if (item < 0) return;
+    const int kvh = head / a.group;
+    const WorkItem it = a.items[item];
     const SeqInfo si = a.seqs[it.seq];
     // the wave index is wave-uniform; readfirstlane lets the compiler keep
     // everything derived from it (row bounds, loop decisions) in scalars
@@ -1060,9 +1056,7 @@ __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
 
 hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s) {
     if (a.n_items == 0) return hipSuccess;
-    // (item, KV head) units padded to a multiple of the 8 XCDs, G query heads each
-    const int64_t units = ((int64_t)a.n_items * a.hkv + 7) / 8 * 8;
-    const dim3 g((unsigned)(units * a.group)), b(256);
+    const dim3 g((unsigned)a.n_wgs), b(256);
     // both pools within the range of one buffer resource
     const uint64_t pool_bytes = (uint64_t)a.num_pages * 16 * a.hkv * head_dim * 2;
     const bool small = pool_bytes <= kSmallPoolBytes;

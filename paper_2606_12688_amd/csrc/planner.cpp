@@ -374,6 +374,58 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     lpt(plan.tiles, true);
     lpt(plan.few, false);
     lpt(plan.f32, true);
+
+    // ---- 6. launch order of the multi-row workgroups ----------------------------
+    // One workgroup per (tile item, query head).  The hardware deals workgroup
+    // b to XCD b % 8, and each XCD has its own L2.  Every workgroup that reads
+    // the same K/V pages -- the items of one request and the G query heads of
+    // one KV head -- goes to the same XCD, consecutively, so they run together
+    // and read each K/V tile from that L2.  Groups go to the least-loaded XCD,
+    // largest first; inside a group the items keep their longest-first order.
+    {
+        struct Group { int64_t cost = 0; int32_t seq = 0, kvh = 0; std::vector<int32_t> items; };
+        std::vector<Group> groups;
+        std::vector<int64_t> index((size_t)num_seqs * P.num_kv_heads, -1);
+        for (size_t i = 0; i < plan.tiles.size(); ++i) {
+            const WorkItem& w = plan.tiles[i];
+            const int64_t pairs = visible_in(w) * G;
+            for (int32_t kvh = 0; kvh < P.num_kv_heads; ++kvh) {
+                int64_t& gi = index[(size_t)w.seq * P.num_kv_heads + kvh];
+                if (gi < 0) {
+                    gi = (int64_t)groups.size();
+                    groups.emplace_back();
+                    groups.back().seq = w.seq;
+                    groups.back().kvh = kvh;
+                }
+                groups[gi].items.push_back((int32_t)i);
+                groups[gi].cost += pairs + 1;  // +1: an empty item still costs a workgroup
+            }
+        }
+        std::stable_sort(groups.begin(), groups.end(), [](const Group& x, const Group& y) { return x.cost > y.cost; });
+        constexpr int kXcds = 8;
+        std::vector<int32_t> lists[kXcds];
+        int64_t load[kXcds] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (const Group& g : groups) {
+            int x = 0;
+            for (int k = 1; k < kXcds; ++k)
+                if (load[k] < load[x]) x = k;
+            load[x] += g.cost;
+            for (int32_t item : g.items)
+                for (int32_t h = g.kvh * G; h < (g.kvh + 1) * G; ++h) {
+                    lists[x].push_back(item);
+                    lists[x].push_back(h);
+                }
+        }
+        size_t slots = 0;
+        for (int x = 0; x < kXcds; ++x) slots = std::max(slots, lists[x].size() / 2);
+        if (slots * kXcds > (size_t)INT32_MAX / 2) { err = "too many tile workgroups"; return MSTAR_ERR_INVALID_ARG; }
+        plan.tile_order.assign(2 * slots * kXcds, -1);  // padding workgroups exit at once
+        for (int x = 0; x < kXcds; ++x)
+            for (size_t k = 0; 2 * k < lists[x].size(); ++k) {
+                plan.tile_order[2 * (k * kXcds + x)] = lists[x][2 * k];
+                plan.tile_order[2 * (k * kXcds + x) + 1] = lists[x][2 * k + 1];
+            }
+    }
     return MSTAR_OK;
 }
 

@@ -21,6 +21,7 @@ struct HostPlan {
     std::vector<int32_t> row_hi;
     std::vector<int32_t> key_lo, key_hi;  // per request union of visible keys
     std::vector<WorkItem> tiles;          // multi-row kernel
+    std::vector<int32_t> tile_order;      // (tile item, query head) of every multi-row workgroup, in launch order
     std::vector<WorkItem> few;            // few-row kernel
     std::vector<WorkItem> f32;            // fp32 kernel
     std::vector<MergeItem> merges;        // (row, head) outputs assembled from partials

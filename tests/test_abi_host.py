@@ -182,3 +182,41 @@ def test_empty_batch_and_zero_query_requests():
     pl = attn.plan(**_params(seqs=np.zeros((0, 3)), masks=np.zeros((0, 3)), segments=np.zeros((0, 4))))
     assert pl.stats()["total_q"] == 0
     pl.destroy()
+
+
+@pytest.mark.parametrize("name", ["text_latent_bf16", "rollout_bf16", "mixed"])
+def test_tile_launch_order_groups_kv_readers_on_one_xcd(name):
+    """Every (tile item, query head) is launched exactly once; all workgroups
+    reading one request's pages for one KV head sit on one XCD (workgroup b
+    runs on XCD b % 8), consecutively; XCD loads differ by at most one group."""
+    b = W.reduced(name) if name == "mixed" else W.FULL_SIZE[name]()
+    pl = plan_for(b, attn.FLAG_HOST_ONLY)
+    items = pl.items(0)
+    order = pl.tile_order()
+    G = b.num_qo_heads // b.num_kv_heads
+    assert len(order) % 8 == 0
+    real = [(i, h) for i, h in order.tolist() if i >= 0]
+    assert all(i == -1 and h == -1 for i, h in order.tolist() if i < 0)
+    assert sorted(real) == sorted((i, h) for i in range(len(items)) for h in range(b.num_qo_heads))
+    xcd_of, pos = {}, {}
+    lists = {x: [] for x in range(8)}
+    for wg, (i, h) in enumerate(order.tolist()):
+        if i < 0:
+            continue
+        grp = (int(items[i][0]), h // G)
+        assert xcd_of.setdefault(grp, wg % 8) == wg % 8
+        lists[wg % 8].append(grp)
+    for x, seq in lists.items():  # a group's workgroups are consecutive on its XCD
+        seen = []
+        for grp in seq:
+            if not seen or seen[-1] != grp:
+                assert grp not in seen, (x, grp)
+                seen.append(grp)
+    sizes = {}
+    for seq in lists.values():
+        for grp in seq:
+            sizes[grp] = sizes.get(grp, 0) + 1
+    counts = [len(seq) for seq in lists.values()]
+    if name != "mixed":  # equal groups: workgroup counts per XCD within one group
+        assert max(counts) - min(counts) <= max(sizes.values())
+    pl.destroy()
