@@ -15,7 +15,8 @@ one step's K/V reads from the previous step.
 
 Prints ONE JSON line.  ``value`` is the whole-job rate in the metric's unit
 for the workload's bound: KV-read GB/s for HBM-bound workloads (decode,
-streaming chunks), useful TFLOP/s for MFMA-bound ones (prefill, rollouts).
+streaming chunks), useful TFLOP/s for MFMA-bound ones (prefill, rollouts, CFG
+labels).
 Useful FLOPs are 4 * head_dim per visible (row, key) pair per query head;
 KV bytes count every distinct visible key of a request and KV head once for
 K and once for V, pages shared between requests once.
@@ -40,11 +41,11 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2516.6   # dense MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
 PEAK_FP32_TFLOPS = 157.3
 BOUND = {"tiny_causal_f32": "alu", "decode_bf16": "hbm", "text_latent_bf16": "mfma",
-         "stream_window_bf16": "hbm", "rollout_bf16": "mfma"}
+         "stream_window_bf16": "hbm", "rollout_bf16": "mfma", "cfg_labels_bf16": "mfma"}
 # kernel classes of mstar_attn_fwd_timed: 0 multi-row tiles, 1 few-row items, 2 fp32, 3 merge
 KERNEL_NAMES = ["tile_kernel", "few_kernel", "f32_kernel", "merge_kernel"]
 DOMINANT = {"tiny_causal_f32": 2, "decode_bf16": 1, "text_latent_bf16": 0, "stream_window_bf16": 1,
-            "rollout_bf16": 0}
+            "rollout_bf16": 0, "cfg_labels_bf16": 0}
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_12688_amd", "csrc", "kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 

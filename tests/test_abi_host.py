@@ -25,7 +25,8 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, name), name
 
 
-WORKLOADS = ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16", "rollout_bf16", "mixed"]
+WORKLOADS = ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16", "rollout_bf16",
+             "cfg_labels_bf16", "mixed"]
 
 
 def _coverage(b, flags):
@@ -184,7 +185,7 @@ def test_empty_batch_and_zero_query_requests():
     pl.destroy()
 
 
-@pytest.mark.parametrize("name", ["text_latent_bf16", "rollout_bf16", "mixed"])
+@pytest.mark.parametrize("name", ["text_latent_bf16", "rollout_bf16", "cfg_labels_bf16", "mixed"])
 def test_tile_launch_order_groups_kv_readers_on_one_xcd(name):
     """Every (tile item, query head) is launched exactly once; all workgroups
     reading one request's pages for one KV head sit on one XCD (workgroup b

@@ -37,7 +37,8 @@ def _oracle(b, t):
     return oracle_attention(b, h["q"], h["k_pages"], h["v_pages"])
 
 
-REDUCED = ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16", "rollout_bf16", "mixed"]
+REDUCED = ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16", "rollout_bf16",
+           "cfg_labels_bf16", "mixed"]
 FLAGS = {"auto": 0, "force_split": attn.FLAG_FORCE_SPLIT, "no_split": attn.FLAG_NO_SPLIT}
 
 
@@ -138,7 +139,7 @@ def test_fwd_rejects_wrong_shapes_and_small_workspace():
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("name", ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16",
-                                  "rollout_bf16"])
+                                  "rollout_bf16", "cfg_labels_bf16"])
 def test_full_size_sampled(name):
     import torch
 

@@ -127,3 +127,31 @@ def test_kv_bytes_count_shared_pages_once():
     c4 = W.stream_window_bf16()
     # 16 rows with windows of 1024 ending at consecutive positions: 1039 distinct keys
     assert useful_work(c4)["kv_bytes"] == 2 * 256 * 1039 * 8 * 128 * 2
+
+
+def test_cfg_labels_see_whole_context_and_alias_text_pages():
+    """Every latent query row of every CFG label sees the label's whole context
+    and its own block; the image-dropped label's text pages are the
+    conditional label's; the text-dropped label shares no page."""
+    text = 32
+    b = W.reduced("cfg_labels_bf16")
+    for r in range(b.num_seqs):
+        q_len, L = int(b.seqs[r, 0]), int(b.seqs[r, 1])
+        assert np.array_equal(_vis(b, r), _brute(q_len, L, lambda p, t: True))
+    tp = text // 16
+    for img in range(b.num_seqs // 3):
+        cond, no_text, no_img = (b.block_table[3 * img + k] for k in range(3))
+        n = [(int(b.seqs[3 * img + k, 1]) + 15) // 16 for k in range(3)]
+        assert np.array_equal(no_img[:tp], cond[:tp])
+        assert not set(no_img[tp:n[2]]) & set(cond[:n[0]])
+        others = set(cond[:n[0]]) | set(no_img[:n[2]])
+        assert not set(no_text[:n[1]]) & others
+
+
+def test_cfg_labels_full_size_counts_closed_form():
+    b = W.cfg_labels_bf16()
+    w = useful_work(b)
+    # 2 images x 28 heads x 4096 latent rows over (256+4096+4096) + (4096+4096) + (256+4096) keys
+    assert w["pairs"] == 2 * 28 * 4096 * (8448 + 8192 + 4352)
+    # distinct keys: per image 8448 + 8192 + 4096 (the text keys of the image-dropped label are shared)
+    assert w["kv_bytes"] == 2 * 2 * (8448 + 8192 + 4096) * 4 * 128 * 2

@@ -279,3 +279,34 @@ def test_sampled_rows_agree_with_scalar_oracle():
         row = int(b.seqs[r, 2]) + i
         np.testing.assert_allclose(ro[n], so[row][h], rtol=0, atol=1e-12)
         assert abs(rl[n] - sl[row][h]) < 1e-12
+
+
+def test_cfg_label_reading_aliased_pages_equals_a_private_copy():
+    """The image-dropped CFG label reads the conditional label's text pages in
+    place; giving it private copies of those pages changes nothing (bitwise),
+    and each label equals unmasked SDPA over its concatenated context."""
+    import dataclasses
+
+    b = W.reduced("cfg_labels_bf16")
+    t = W.make_tensors_numpy(b)
+    o1, l1 = oracle_attention(b, t["q"], t["k_pages"], t["v_pages"])
+    tp = 32 // 16
+    bt = b.block_table.copy()
+    k, v = t["k_pages"], t["v_pages"]
+    extra_k, extra_v = [], []
+    for r in range(2, b.num_seqs, 3):
+        for j in range(tp):
+            src = int(bt[r, j])
+            extra_k.append(k[src]); extra_v.append(v[src])
+            bt[r, j] = b.num_pages + len(extra_k) - 1
+    b2 = dataclasses.replace(b, block_table=bt, num_pages=b.num_pages + len(extra_k))
+    k2 = np.concatenate([k, np.stack(extra_k)]); v2 = np.concatenate([v, np.stack(extra_v)])
+    o2, l2 = oracle_attention(b2, t["q"], k2, v2)
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+    for r in range(b.num_seqs):
+        q_len, L, qs = (int(x) for x in b.seqs[r])
+        K, V = _contiguous(b, t, r)
+        q = t["q"][qs:qs + q_len].astype(np.float64)
+        ro, rl = _sdpa(q, K, V, b.sm_scale, gqa=True)
+        np.testing.assert_allclose(o1[qs:qs + q_len], ro, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(l1[qs:qs + q_len], rl, rtol=0, atol=1e-12)

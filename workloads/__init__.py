@@ -22,6 +22,12 @@ per-layer attention shapes and its datasets are not used):
 * ``rollout_bf16``      - K candidate rollouts appending frame blocks over one
                           shared context whose pages every block table points
                           to (V-JEPA 2 rollout and MPC, Sec. 4.4 and App. A).
+* ``cfg_labels_bf16``   - an image-editing flow step under classifier-free
+                          guidance: the three CFG contexts (conditional,
+                          text dropped, image dropped) as three labels over
+                          one paged pool, the image-dropped label reading the
+                          conditional label's text pages in place (Sec. 4.1;
+                          App. F, CFG Walk).
 * ``mixed``             - requests of all the kinds above in one launch (one
                           ``LLM`` replica serving every Walk, Sec. 3.2).
 
@@ -200,6 +206,49 @@ def rollout_bf16(seed: int = 0, n: int = 300, prefix: int = 2048, frames: int = 
     return _finish("rollout_bf16", hq, hkv, d, "bf16", [q] * n, kv, segs, [0] * n, bt, pool, seed)
 
 
+def cfg_labels_bf16(seed: int = 0, n: int = 2, text: int = 256, image: int = 4096, latent: int = 4096,
+                    hq: int = 28, hkv: int = 4, d: int = 128) -> Batch:
+    """n image-editing requests at one flow step, each as three CFG labels over
+    one page pool; in every label the ``latent`` tokens are the queries and form
+    one full-attention block that sees the label's whole context:
+
+    * conditional:   causal text (``text``), full condition image (``image``), latents;
+    * text dropped:  full condition image (its own pages), latents;
+    * image dropped: causal text, latents.  Its text pages are the conditional
+      label's text pages (the same causal prefix, read in place).
+
+    Requests are ordered image by image: conditional, text dropped, image dropped.
+    """
+    if text % PAGE:
+        raise ValueError("the shared text prefix must be page aligned")
+    rng = _rng(seed, _SUB_PERM)
+    q_lens, kv_lens, seg_lists = [], [], []
+    for _ in range(n):
+        q_lens += [latent] * 3
+        kv_lens += [text + image + latent, image + latent, text + latent]
+        seg_lists += [
+            [(0, text, SEG_CAUSAL, 0), (text, image, SEG_FULL, 0), (text + image, latent, SEG_FULL, 0)],
+            [(0, image, SEG_FULL, 0), (image, latent, SEG_FULL, 0)],
+            [(0, text, SEG_CAUSAL, 0), (text, latent, SEG_FULL, 0)],
+        ]
+    need = [(x + PAGE - 1) // PAGE for x in kv_lens]
+    tp = text // PAGE
+    own = [need[r] - (tp if r % 3 == 2 else 0) for r in range(len(need))]
+    pool = sum(own)
+    perm = rng.permutation(pool).astype(np.int32)
+    bt = np.full((len(kv_lens), max(need)), -1, dtype=np.int32)
+    cur = 0
+    for r in range(len(kv_lens)):
+        if r % 3 == 2:  # image dropped: the conditional label's text pages, then its own
+            bt[r, :tp] = bt[r - 2, :tp]
+            bt[r, tp:tp + own[r]] = perm[cur:cur + own[r]]
+        else:
+            bt[r, :own[r]] = perm[cur:cur + own[r]]
+        cur += own[r]
+    return _finish("cfg_labels_bf16", hq, hkv, d, "bf16", q_lens, kv_lens, seg_lists, [0] * len(q_lens),
+                   bt, pool, seed)
+
+
 def mixed(seed: int = 0, hq: int = 8, hkv: int = 2, d: int = 128, dtype: str = "bf16",
           scale: int = 1) -> Batch:
     """Requests of every kind in one launch: decode, text+latent prefill,
@@ -257,6 +306,7 @@ FULL_SIZE = {
     "text_latent_bf16": text_latent_bf16,
     "stream_window_bf16": stream_window_bf16,
     "rollout_bf16": rollout_bf16,
+    "cfg_labels_bf16": cfg_labels_bf16,
 }
 
 
@@ -274,6 +324,8 @@ def reduced(name: str, seed: int = 0) -> Batch:
         return stream_window_bf16(seed, n=7, cmin=1, cmax=700, window=100)
     if name == "rollout_bf16":
         return rollout_bf16(seed, n=5, prefix=64, frames=4, frame=40)
+    if name == "cfg_labels_bf16":
+        return cfg_labels_bf16(seed, n=2, text=32, image=101, latent=70, hq=7, hkv=1)
     if name == "mixed":
         return mixed(seed)
     raise KeyError(name)
