@@ -13,7 +13,9 @@ table, plus the natural-log log-sum-exp of the scaled scores.  The paper runs
 this computation through a paged-attention library inside its
 ``KVCacheEngine`` (Sec. 3.3, Runtime) over one shared page pool whose page
 tables are read in place (Sec. 4.1); it does not define the masks, so the
-mask semantics are the reading stated in ``attention.py``.
+mask semantics are the reading stated in ``attention.py``.  ``append.py``
+holds the paged KV append (the step's new K/V rows written into their pages
+before attention reads them).
 
 Pins (tests marked ``not gpu``): brute-force visibility predicates written from
 each workload's wording, torch's CPU float64 ``scaled_dot_product_attention``
@@ -36,3 +38,4 @@ from .attention import (  # noqa: F401
     useful_work,
     visible_matrix,
 )
+from .append import append_targets, kv_append  # noqa: F401
