@@ -112,6 +112,60 @@ def cpu_baseline(b, tensors, unit, budget_s=15.0):
             "host_threads_available": len(os.sched_getaffinity(0))}
 
 
+def bench_append(args, b, dev):
+    """Time ``mstar_kv_append`` alone: every new K and V row of the workload is
+    read once and written once (HBM-bound); one JSON line."""
+    import torch
+
+    import workloads as W
+    from paper_2606_12688_amd import attn
+
+    stream = torch.cuda.current_stream()
+    pl = attn.plan(b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, b.seqs, b.masks, b.segments,
+                   b.block_table.shape[1], b.num_pages, b.sm_scale, 0, stream)
+    t = W.make_tensors_torch(b, dev, seed=args.seed)
+    g = torch.Generator(device=dev)
+    g.manual_seed(args.seed + 77)
+    shape = (b.total_q, b.num_kv_heads, b.head_dim)
+    dt = t["q"].dtype
+    kn = torch.randn(shape, generator=g, device=dev).to(dt)
+    vn = torch.randn(shape, generator=g, device=dev).to(dt)
+    bt = torch.from_numpy(np.ascontiguousarray(b.block_table)).to(dev)
+    attn.kv_append(pl, kn, vn, bt, t["k_pages"], t["v_pages"], stream)
+    assert attn.check(pl, stream) == 0
+    L = attn.lib()
+    call = (pl.handle, kn.data_ptr(), vn.data_ptr(), bt.data_ptr(), t["k_pages"].data_ptr(),
+            t["v_pages"].data_ptr(), stream.cuda_stream)
+    for _ in range(args.warmup):
+        L.mstar_kv_append(*call)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        rc = L.mstar_kv_append(*call)
+        if rc != 0:
+            raise attn.MStarError(rc, attn.last_error())
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / args.steps
+    kernel_ms = e0.elapsed_time(e1) / args.steps
+    assert attn.check(pl, stream) == 0
+    esize = 4 if b.dtype == "f32" else 2
+    nbytes = 2 * 2 * b.total_q * b.num_kv_heads * b.head_dim * esize  # K and V, read and written
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    achieved = nbytes / (kernel_ms * 1e-3) / 1e9
+    print(json.dumps({
+        "metric": "paged KV append HBM GB/s (new K/V rows read and written)", "value": round(gbs, 3),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": b.dtype, "data": "synthetic",
+        "config": dict(describe(b), op="kv_append", new_rows=b.total_q),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 3), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None},
+        "bytes_per_step": nbytes}), flush=True)
+    pl.destroy()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -120,6 +174,8 @@ def main():
     ap.add_argument("--workload", default="decode_bf16", choices=sorted(BOUND))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--op", default="attention", choices=["attention", "append"],
+                    help="append: time mstar_kv_append (the step's new K/V rows into their pages) instead")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (for HBM counter calibration)")
     args = ap.parse_args()
@@ -149,6 +205,9 @@ def main():
     from paper_2606_12688_amd import attn
 
     b = W.FULL_SIZE[args.workload](args.seed)
+    if args.op == "append":
+        bench_append(args, b, dev)
+        return
     bound = BOUND[args.workload]
     stream = torch.cuda.current_stream()
     def make_plan():

@@ -212,6 +212,30 @@ int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, int32_t* items
  * request's pages for one KV head share an XCD.  For inspection and tests. */
 int mstar_attn_plan_tile_order(const mstar_plan_t* plan, int32_t* pairs, int64_t capacity, int64_t* count);
 
+/* Paged KV append: write the step's new key and value rows into their pages
+ * before attention reads them.  Each node execution of the paper's
+ * transformer engine stores the K/V of the tokens it processes in the paged
+ * cache and then attends over it (Sec. 3.3, Runtime; Sec. 4.4: rollouts reuse
+ * the paged cache instead of re-prefilling).
+ *
+ * For request r of the plan, packed row q_start + i of k_new / v_new
+ * ([total_q][num_kv_heads][head_dim], the plan's dtype; the same row
+ * numbering as q) holds the key / value of position kv_len - q_len + i, the
+ * position of its query row; it is copied to page block_table[r][pos / 16],
+ * slot pos % 16 of k_pages / v_pages (NHD layout as in mstar_attn_fwd).  No
+ * other slot is written.  Two new rows must not target one slot (pages shared
+ * between requests hold cached positions, not new ones); if they do, which one
+ * lands is unspecified.  A target page outside [0, num_pages) is skipped and
+ * sets MSTAR_DEVERR_PAGE_RANGE in the plan's error word (mstar_attn_check).
+ *
+ * All pointers are caller-owned device memory; k_new, v_new, k_pages and
+ * v_pages must be 16-byte aligned.  Enqueued on `stream` with no allocation
+ * and no host synchronisation; an attention call on the same stream afterwards
+ * sees the new rows.  Returns MSTAR_OK (also when the plan has no new rows) or
+ * a negative code. */
+int mstar_kv_append(const mstar_plan_t* plan, const void* k_new, const void* v_new, const int32_t* block_table,
+                    void* k_pages, void* v_pages, void* stream);
+
 /* Release the plan (host and device memory).  The caller guarantees no
  * enqueued fwd still uses it.  NULL is ignored. */
 void mstar_attn_plan_destroy(mstar_plan_t* plan);

@@ -3,7 +3,8 @@
 Argument marshalling only: every step of the computation runs in the HIP
 library.  PyTorch supplies device memory and streams.  The names follow the C
 entry points: :func:`plan` (``mstar_attn_plan``), :meth:`Plan.workspace_bytes`,
-:func:`fwd` (``mstar_attn_fwd``), :func:`check` (``mstar_attn_check``),
+:func:`fwd` (``mstar_attn_fwd``), :func:`kv_append` (``mstar_kv_append``),
+:func:`check` (``mstar_attn_check``),
 :meth:`Plan.stats`, :meth:`Plan.key_ranges`, :meth:`Plan.items`,
 :meth:`Plan.destroy` and :func:`last_error`.
 
@@ -42,6 +43,7 @@ EXPORTS = [
     "mstar_attn_plan_key_ranges",
     "mstar_attn_plan_items",
     "mstar_attn_plan_tile_order",
+    "mstar_kv_append",
     "mstar_attn_plan_destroy",
     "mstar_last_error",
 ]
@@ -111,6 +113,8 @@ def lib() -> ctypes.CDLL:
     L.mstar_attn_plan_items.restype = ctypes.c_int
     L.mstar_attn_plan_tile_order.argtypes = [vp, vp, i64, ctypes.POINTER(i64)]
     L.mstar_attn_plan_tile_order.restype = ctypes.c_int
+    L.mstar_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, vp]
+    L.mstar_kv_append.restype = ctypes.c_int
     L.mstar_attn_plan_destroy.argtypes = [vp]
     L.mstar_attn_plan_destroy.restype = None
     L.mstar_last_error.argtypes = []
@@ -266,6 +270,29 @@ def fwd(pl: Plan, q, k_pages, v_pages, block_table, out, lse, workspace=None, st
     _check_rc(lib().mstar_attn_fwd(pl.handle, q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
                                    block_table.data_ptr(), out.data_ptr(), lse.data_ptr(), ws_ptr, ws_bytes,
                                    _stream_handle(stream)))
+
+
+def kv_append(pl: Plan, k_new, v_new, block_table, k_pages, v_pages, stream=None):
+    """``mstar_kv_append`` on torch tensors: write the plan's new K/V rows
+    (``[total_q, Hkv, d]``, the same row numbering as q) into their pages."""
+    import torch
+
+    p = pl.params
+    dt = torch.float32 if p.dtype == DTYPE_F32 else torch.bfloat16
+    dev = k_new.device
+    for name, t in (("k_new", k_new), ("v_new", v_new), ("block_table", block_table), ("k_pages", k_pages),
+                    ("v_pages", v_pages)):
+        _need(t.is_cuda and t.device == dev, f"{name} must be on {dev}")
+        _need(t.is_contiguous(), f"{name} must be contiguous")
+    _need(k_new.dtype == dt and v_new.dtype == dt and k_pages.dtype == dt and v_pages.dtype == dt, "dtype mismatch")
+    row = (pl.total_q, p.num_kv_heads, p.head_dim)
+    _need(tuple(k_new.shape) == row and tuple(v_new.shape) == row, f"k_new/v_new must be {list(row)}")
+    kv_shape = (p.num_pages, p.page_size, p.num_kv_heads, p.head_dim)
+    _need(tuple(k_pages.shape) == kv_shape and tuple(v_pages.shape) == kv_shape, f"pages must be {kv_shape}")
+    _need(block_table.dtype == torch.int32 and tuple(block_table.shape) == (pl.num_seqs, p.max_blocks_per_seq),
+          f"block_table must be int32 [{pl.num_seqs}, {p.max_blocks_per_seq}]")
+    _check_rc(lib().mstar_kv_append(pl.handle, k_new.data_ptr(), v_new.data_ptr(), block_table.data_ptr(),
+                                    k_pages.data_ptr(), v_pages.data_ptr(), _stream_handle(stream)))
 
 
 def check(pl: Plan, stream=None) -> int:

@@ -20,7 +20,7 @@ struct mstar_plan {
     void* dev = nullptr;     // device copy of the plan blob
     void* pinned = nullptr;  // pinned staging copy (kept until destroy)
     size_t bytes = 0;
-    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_order = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_err = 0;
+    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_order = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_append = 0, off_err = 0;
     double plan_us = 0.0;
 };
 
@@ -80,7 +80,7 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     }
     const mstar::HostPlan& h = plan->host;
 
-    // blob layout: seqs | row_hi | tiles | tile order | few | f32 | merges | error word
+    // blob layout: seqs | row_hi | tiles | tile order | few | f32 | merges | appends | error word
     size_t off = 0;
     plan->off_seqs = off;   off = align256(off + h.seqs.size() * sizeof(mstar::SeqInfo));
     plan->off_row_hi = off; off = align256(off + h.row_hi.size() * sizeof(int32_t));
@@ -89,6 +89,7 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     plan->off_few = off;    off = align256(off + h.few.size() * sizeof(mstar::WorkItem));
     plan->off_f32 = off;    off = align256(off + h.f32.size() * sizeof(mstar::WorkItem));
     plan->off_merge = off;  off = align256(off + h.merges.size() * sizeof(mstar::MergeItem));
+    plan->off_append = off; off = align256(off + h.appends.size() * sizeof(mstar::WorkItem));
     plan->off_err = off;    off = align256(off + sizeof(int32_t));
     plan->bytes = off;
 
@@ -107,6 +108,7 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
         put(blob, plan->off_few, h.few);
         put(blob, plan->off_f32, h.f32);
         put(blob, plan->off_merge, h.merges);
+        put(blob, plan->off_append, h.appends);
         e = hipMalloc(&plan->dev, plan->bytes);
         if (e != hipSuccess) {
             (void)hipHostFree(plan->pinned);
@@ -229,6 +231,37 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
         MSTAR_MARK(events_after, 3);
     }
 #undef MSTAR_MARK
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_kv_append(const mstar_plan_t* plan, const void* k_new, const void* v_new,
+                                 const int32_t* block_table, void* k_pages, void* v_pages, void* stream) {
+    if (!plan) return fail(MSTAR_ERR_INVALID_ARG, "plan is NULL");
+    if (!plan->dev) return fail(MSTAR_ERR_INVALID_ARG, "plan was built host-only");
+    const mstar::HostPlan& h = plan->host;
+    if (h.appends.empty()) return MSTAR_OK;
+    if (!k_new || !v_new || !block_table || !k_pages || !v_pages)
+        return fail(MSTAR_ERR_INVALID_ARG, "a tensor pointer is NULL");
+    if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_pages, 16) || !aligned(v_pages, 16) ||
+        !aligned(block_table, 4))
+        return fail(MSTAR_ERR_INVALID_ARG, "k_new/v_new/k_pages/v_pages must be 16-byte aligned");
+    unsigned char* blob = static_cast<unsigned char*>(plan->dev);
+    mstar::AArgs a{};
+    a.seqs = reinterpret_cast<const mstar::SeqInfo*>(blob + plan->off_seqs);
+    a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_append);
+    a.k_new = k_new;
+    a.v_new = v_new;
+    a.bt = block_table;
+    a.k = k_pages;
+    a.v = v_pages;
+    a.err = reinterpret_cast<int32_t*>(blob + plan->off_err);
+    a.n_items = (int32_t)h.appends.size();
+    const int elt = h.params.dtype == MSTAR_DTYPE_BF16 ? 2 : 4;
+    a.row_bytes = h.params.num_kv_heads * h.params.head_dim * elt;
+    a.bt_stride = h.params.max_blocks_per_seq;
+    a.num_pages = h.params.num_pages;
+    hipError_t e = mstar::launch_append(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "append kernel launch");
     return MSTAR_OK;
 }
 

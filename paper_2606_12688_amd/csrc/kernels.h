@@ -38,7 +38,22 @@ struct MArgs {
     int32_t hq;
 };
 
+struct AArgs {
+    const SeqInfo* seqs;
+    const WorkItem* items;  // KV append items: rows row0 .. row0 + nrows - 1 of request seq
+    const void* k_new;      // [total_q][row_bytes]
+    const void* v_new;
+    const int32_t* bt;
+    void* k;                // pages [num_pages][16][row_bytes]
+    void* v;
+    int32_t* err;           // sticky device error word
+    int32_t n_items;
+    int32_t row_bytes;      // Hkv * head_dim * element size (a multiple of 16)
+    int32_t bt_stride, num_pages;
+};
+
 hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_append(const AArgs& a, hipStream_t s);
 hipError_t launch_few(const KArgs& a, int head_dim, int row_blocks, hipStream_t s);
 hipError_t launch_f32(const KArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_merge(const MArgs& a, int head_dim, bool bf16_out, hipStream_t s);

@@ -1052,7 +1052,50 @@ __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
     if (lane == 0) a.lse[row] = tot > 0.0f ? mstar + logf(tot) : kNegInf;
 }
 
+// ---------------------------------------------------------------------------
+// KV append: one workgroup per item of up to 16 new rows of one request; wave
+// w copies rows w, w + 4, ...  A row is one token's keys (or values) for
+// every KV head, contiguous in both the packed input and the page slot, so
+// lanes copy it in 16-byte pieces.  A target page outside the pool is
+// skipped and sets the error word.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void append_kernel(AArgs a) {
+    const WorkItem it = a.items[blockIdx.x];
+    const SeqInfo si = a.seqs[it.seq];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & 3, lane = threadIdx.x & 63;
+    const int chunks = a.row_bytes >> 4;
+    const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
+    bool bad = false;
+    for (int r = wave; r < it.nrows; r += 4) {
+        const int32_t i = it.row0 + r;                 // new row within the request
+        const int32_t pos = si.kv_len - si.q_len + i;  // its position in the cache
+        const int32_t page = bt_row[pos >> 4];
+        if ((uint32_t)page >= (uint32_t)a.num_pages) {
+            bad = true;
+            continue;
+        }
+        const int64_t src = (int64_t)(si.q_start + i) * a.row_bytes;
+        const int64_t dst = ((int64_t)page * 16 + (pos & 15)) * a.row_bytes;
+        const uint4* ks = reinterpret_cast<const uint4*>(static_cast<const char*>(a.k_new) + src);
+        const uint4* vs = reinterpret_cast<const uint4*>(static_cast<const char*>(a.v_new) + src);
+        uint4* kd = reinterpret_cast<uint4*>(static_cast<char*>(a.k) + dst);
+        uint4* vd = reinterpret_cast<uint4*>(static_cast<char*>(a.v) + dst);
+        for (int c = lane; c < chunks; c += 64) {
+            const uint4 kx = ks[c], vx = vs[c];
+            kd[c] = kx;
+            vd[c] = vx;
+        }
+    }
+    if (bad && lane == 0) atomicOr(a.err, MSTAR_DEVERR_PAGE_RANGE_BIT);
+}
+
 }  // namespace
+
+hipError_t launch_append(const AArgs& a, hipStream_t s) {
+    if (a.n_items == 0) return hipSuccess;
+    hipLaunchKernelGGL(append_kernel, dim3(a.n_items), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
 
 hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s) {
     if (a.n_items == 0) return hipSuccess;

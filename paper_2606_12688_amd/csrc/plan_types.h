@@ -11,6 +11,7 @@ constexpr int kTileKeys = 64;      // keys per LDS tile in the multi-row kernel
 constexpr int kDecodeMaxRows = 64; // (query row x head) rows a few-row item may hold
 constexpr int kSubKeys = 32;       // keys per wave step in the few-row kernel
 constexpr int kF32Rows = 4;        // query rows per fp32 item (one wave each)
+constexpr int kAppendRows = 16;    // new K/V rows per KV-append item
 
 // Per request.  Query row i sits at position kv_len - q_len + i; its visible
 // keys are [lo(i), hi(i)) with hi(i) = row_hi[hi_off + i] and

@@ -274,6 +274,16 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         }
     }
 
+    // KV append items: the new rows of each request in chunks of kAppendRows
+    for (int32_t r = 0; r < num_seqs; ++r) {
+        const mstar_seq_desc& s = seqs[r];
+        for (int32_t row0 = 0; row0 < s.q_len; row0 += kAppendRows) {
+            const int32_t nr = std::min(kAppendRows, s.q_len - row0);
+            plan.appends.push_back(WorkItem{r, -1, row0, nr, s.kv_len - s.q_len + row0, s.kv_len - s.q_len + row0 + nr,
+                                            -1, -1});
+        }
+    }
+
     // ---- 4. key splitting ---------------------------------------------------
     int64_t slot = 0;
     // Few-row units are cut into pieces of exactly `chunk` keys plus one shorter

@@ -25,6 +25,7 @@ struct HostPlan {
     std::vector<WorkItem> few;            // few-row kernel
     std::vector<WorkItem> f32;            // fp32 kernel
     std::vector<MergeItem> merges;        // (row, head) outputs assembled from partials
+    std::vector<WorkItem> appends;        // KV append: up to kAppendRows new rows of one request each
     int64_t visible_pairs = 0;
     int64_t partial_slots = 0;
 };
