@@ -166,6 +166,66 @@ def bench_append(args, b, dev):
     pl.destroy()
 
 
+def bench_serve(args, b, dev):
+    """A serving loop over one workload: every step plans the batch again (the
+    batch changes from step to step in a server), runs the attention and waits
+    for it (standing in for reading back the step's tokens).  Inline: plan,
+    then attention, on the critical path.  Async: the plan of step i+1 is built
+    on the planner's thread and stream while step i runs (Sec. 3.3, Runtime).
+    One JSON line with the per-step wall time of both."""
+    import torch
+
+    import workloads as W
+    from paper_2606_12688_amd import attn
+
+    stream = torch.cuda.current_stream()
+    t = W.make_tensors_torch(b, dev, seed=args.seed)
+    out = torch.empty_like(t["q"])
+    lse = torch.empty(t["q"].shape[:2], dtype=torch.float32, device=dev)
+    bt = torch.from_numpy(np.ascontiguousarray(b.block_table)).to(dev)
+    args_plan = (b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, b.seqs, b.masks, b.segments,
+                 b.block_table.shape[1], b.num_pages, b.sm_scale, 0)
+    pl0 = attn.plan(*args_plan, stream)
+    ws = attn.workspace(pl0, dev)  # the same shapes every step: one workspace
+    pl0.destroy()
+
+    def inline(n):
+        for _ in range(n):
+            pl = attn.plan(*args_plan, stream)
+            attn.fwd(pl, t["q"], t["k_pages"], t["v_pages"], bt, out, lse, ws, stream)
+            torch.cuda.synchronize()
+            pl.destroy()
+
+    ap = attn.AsyncPlanner(depth=2)
+
+    def overlapped(n):
+        ap.submit(*args_plan)
+        for i in range(n):
+            if i + 1 < n:
+                ap.submit(*args_plan)
+            pl = ap.take(stream)
+            attn.fwd(pl, t["q"], t["k_pages"], t["v_pages"], bt, out, lse, ws, stream)
+            torch.cuda.synchronize()
+            pl.destroy()
+
+    res = {}
+    for name, fn in (("inline", inline), ("async", overlapped)):
+        fn(args.warmup)
+        t0 = time.perf_counter()
+        fn(args.steps)
+        res[name] = (time.perf_counter() - t0) * 1e3 / args.steps
+    ap.close()
+    st = attn.plan(*args_plan[:-1], attn.FLAG_HOST_ONLY)
+    plan_us = st.stats()["plan_host_us"]
+    st.destroy()
+    print(json.dumps({
+        "metric": "serving-loop step time, plan + attention + wait (ms)", "value": round(res["async"], 5),
+        "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(res["async"], 5),
+        "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": b.dtype, "data": "synthetic",
+        "config": dict(describe(b), op="serve"), "inline_ms_per_step": round(res["inline"], 5),
+        "async_ms_per_step": round(res["async"], 5), "plan_host_us": round(plan_us, 1)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -174,8 +234,9 @@ def main():
     ap.add_argument("--workload", default="decode_bf16", choices=sorted(BOUND))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op", default="attention", choices=["attention", "append"],
-                    help="append: time mstar_kv_append (the step's new K/V rows into their pages) instead")
+    ap.add_argument("--op", default="attention", choices=["attention", "append", "serve"],
+                    help="append: time mstar_kv_append (the step's new K/V rows into their pages); serve: a "
+                         "serving loop that re-plans every step, planning inline vs on the async planner")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain 1 GiB device copy (for HBM counter calibration)")
     args = ap.parse_args()
@@ -207,6 +268,9 @@ def main():
     b = W.FULL_SIZE[args.workload](args.seed)
     if args.op == "append":
         bench_append(args, b, dev)
+        return
+    if args.op == "serve":
+        bench_serve(args, b, dev)
         return
     bound = BOUND[args.workload]
     stream = torch.cuda.current_stream()

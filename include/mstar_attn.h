@@ -111,6 +111,7 @@ typedef struct {
 } mstar_attn_params;
 
 typedef struct mstar_plan mstar_plan_t;
+typedef struct mstar_planner mstar_planner_t;
 
 typedef struct {
     int64_t visible_pairs;   /* (row, key) pairs the rows may see, summed over query heads */
@@ -211,6 +212,36 @@ int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, int32_t* items
  * workgroup.  Workgroup b runs on XCD b % 8; all workgroups that read one
  * request's pages for one KV head share an XCD.  For inspection and tests. */
 int mstar_attn_plan_tile_order(const mstar_plan_t* plan, int32_t* pairs, int64_t capacity, int64_t* count);
+
+/* Asynchronous, double-buffered planning.  The paper's workers build the
+ * attention plan of the next batch on a separate thread and stream while the
+ * current batch runs, since planning is often the heaviest CPU overhead of a
+ * step (Sec. 3.3, Runtime).  A planner owns one worker thread and one HIP
+ * stream (default priority) for the uploads.
+ *
+ * mstar_planner_create: `depth` (1..64, normally 2) is the number of plans
+ *   that may be submitted and not yet taken.
+ * mstar_planner_submit: copies the descriptors (same meaning and checks as
+ *   mstar_attn_plan; the device is the calling thread's current one) and
+ *   returns at once, unless `depth` plans are outstanding, in which case it
+ *   waits until one is taken.  Plans are built in submission order.
+ * mstar_planner_take: waits for the oldest outstanding plan, makes `stream`
+ *   wait (on the device, no host sync) for its upload, and returns it; the
+ *   caller owns it (mstar_attn_plan_destroy).  A planning error is returned
+ *   here with its message.  MSTAR_ERR_INVALID_ARG if nothing is outstanding.
+ * mstar_attn_plan_wait: makes `stream` wait for a planner-built plan's upload
+ *   (a plan from mstar_attn_plan has none to wait for: its upload is ordered
+ *   by the stream it was given).  Not for use inside graph capture.
+ * mstar_planner_destroy: finishes queued work, destroys untaken plans and
+ *   the stream.  Submit and take may be called from different threads; one
+ *   planner must not be destroyed while another thread uses it. */
+int mstar_planner_create(int32_t depth, mstar_planner_t** out);
+int mstar_planner_submit(mstar_planner_t* planner, const mstar_attn_params* params, const mstar_seq_desc* seqs,
+                         const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segments,
+                         int32_t num_segs);
+int mstar_planner_take(mstar_planner_t* planner, void* stream, mstar_plan_t** out);
+int mstar_attn_plan_wait(const mstar_plan_t* plan, void* stream);
+void mstar_planner_destroy(mstar_planner_t* planner);
 
 /* Paged KV append: write the step's new key and value rows into their pages
  * before attention reads them.  Each node execution of the paper's

@@ -5,7 +5,7 @@ library.  PyTorch supplies device memory and streams.  The names follow the C
 entry points: :func:`plan` (``mstar_attn_plan``), :meth:`Plan.workspace_bytes`,
 :func:`fwd` (``mstar_attn_fwd``), :func:`kv_append` (``mstar_kv_append``),
 :func:`check` (``mstar_attn_check``),
-:meth:`Plan.stats`, :meth:`Plan.key_ranges`, :meth:`Plan.items`,
+:class:`AsyncPlanner` (``mstar_planner_*``), :meth:`Plan.stats`, :meth:`Plan.key_ranges`, :meth:`Plan.items`,
 :meth:`Plan.destroy` and :func:`last_error`.
 
 If ``libmstar_attn.so`` has not been built, loading fails loudly; there is no
@@ -44,6 +44,11 @@ EXPORTS = [
     "mstar_attn_plan_items",
     "mstar_attn_plan_tile_order",
     "mstar_kv_append",
+    "mstar_planner_create",
+    "mstar_planner_submit",
+    "mstar_planner_take",
+    "mstar_attn_plan_wait",
+    "mstar_planner_destroy",
     "mstar_attn_plan_destroy",
     "mstar_last_error",
 ]
@@ -115,6 +120,17 @@ def lib() -> ctypes.CDLL:
     L.mstar_attn_plan_tile_order.restype = ctypes.c_int
     L.mstar_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, vp]
     L.mstar_kv_append.restype = ctypes.c_int
+    L.mstar_planner_create.argtypes = [i32, ctypes.POINTER(vp)]
+    L.mstar_planner_create.restype = ctypes.c_int
+    L.mstar_planner_submit.argtypes = [vp, ctypes.POINTER(Params), ctypes.POINTER(SeqDesc), ctypes.POINTER(MaskSpec),
+                                       i32, ctypes.POINTER(Segment), i32]
+    L.mstar_planner_submit.restype = ctypes.c_int
+    L.mstar_planner_take.argtypes = [vp, vp, ctypes.POINTER(vp)]
+    L.mstar_planner_take.restype = ctypes.c_int
+    L.mstar_attn_plan_wait.argtypes = [vp, vp]
+    L.mstar_attn_plan_wait.restype = ctypes.c_int
+    L.mstar_planner_destroy.argtypes = [vp]
+    L.mstar_planner_destroy.restype = None
     L.mstar_attn_plan_destroy.argtypes = [vp]
     L.mstar_attn_plan_destroy.restype = None
     L.mstar_last_error.argtypes = []
@@ -211,11 +227,8 @@ class Plan:
             pass
 
 
-def plan(num_qo_heads: int, num_kv_heads: int, head_dim: int, dtype: str, seqs, masks, segments,
-         max_blocks_per_seq: int, num_pages: int, sm_scale: Optional[float] = None, flags: int = 0,
-         stream=None, page_size: int = 16) -> Plan:
-    """``mstar_attn_plan``: ``seqs [n,3]`` (q_len, kv_len, q_start), ``masks [n,3]``
-    (seg_begin, seg_count, window), ``segments [S,4]`` (start, len, kind, block)."""
+def _descriptors(num_qo_heads, num_kv_heads, head_dim, dtype, seqs, masks, segments, max_blocks_per_seq,
+                 num_pages, sm_scale, flags, page_size):
     p = Params()
     p.num_qo_heads, p.num_kv_heads, p.head_dim, p.page_size = num_qo_heads, num_kv_heads, head_dim, page_size
     p.dtype = {"f32": DTYPE_F32, "bf16": DTYPE_BF16}[dtype] if isinstance(dtype, str) else int(dtype)
@@ -226,12 +239,65 @@ def plan(num_qo_heads: int, num_kv_heads: int, head_dim: int, dtype: str, seqs, 
     g_arr, ns = _array(Segment, segments, 4)
     if nm != n:
         raise ValueError("seqs and masks differ in length")
+    sq = np.asarray(seqs, dtype=np.int64).reshape(-1, 3)
+    total_q = int((sq[:, 0] + sq[:, 2]).max()) if n else 0
+    return p, s_arr, n, m_arr, g_arr, ns, total_q
+
+
+def plan(num_qo_heads: int, num_kv_heads: int, head_dim: int, dtype: str, seqs, masks, segments,
+         max_blocks_per_seq: int, num_pages: int, sm_scale: Optional[float] = None, flags: int = 0,
+         stream=None, page_size: int = 16) -> Plan:
+    """``mstar_attn_plan``: ``seqs [n,3]`` (q_len, kv_len, q_start), ``masks [n,3]``
+    (seg_begin, seg_count, window), ``segments [S,4]`` (start, len, kind, block)."""
+    p, s_arr, n, m_arr, g_arr, ns, total_q = _descriptors(num_qo_heads, num_kv_heads, head_dim, dtype, seqs, masks,
+                                                          segments, max_blocks_per_seq, num_pages, sm_scale,
+                                                          flags, page_size)
     h = ctypes.c_void_p(None)
     stream_h = None if flags & FLAG_HOST_ONLY else _stream_handle(stream)
     _check_rc(lib().mstar_attn_plan(ctypes.byref(p), s_arr, m_arr, n, g_arr, ns, stream_h, ctypes.byref(h)))
-    sq = np.asarray(seqs, dtype=np.int64).reshape(-1, 3)
-    total_q = int((sq[:, 0] + sq[:, 2]).max()) if n else 0
     return Plan(h.value, p, n, total_q)
+
+
+class AsyncPlanner:
+    """``mstar_planner_*``: plans built in submission order on a native worker
+    thread with its own HIP stream, at most ``depth`` outstanding (double
+    buffering with the default 2).  :meth:`submit` takes the arguments of
+    :func:`plan` (without ``stream``); :meth:`take` returns the oldest plan
+    after making ``stream`` wait for its upload."""
+
+    def __init__(self, depth: int = 2):
+        h = ctypes.c_void_p(None)
+        _check_rc(lib().mstar_planner_create(int(depth), ctypes.byref(h)))
+        self._h = h
+        self._pending = []
+
+    def submit(self, num_qo_heads, num_kv_heads, head_dim, dtype, seqs, masks, segments, max_blocks_per_seq,
+               num_pages, sm_scale=None, flags=0, page_size=16):
+        p, s_arr, n, m_arr, g_arr, ns, total_q = _descriptors(num_qo_heads, num_kv_heads, head_dim, dtype, seqs,
+                                                              masks, segments, max_blocks_per_seq, num_pages,
+                                                              sm_scale, flags, page_size)
+        _check_rc(lib().mstar_planner_submit(self._h, ctypes.byref(p), s_arr, m_arr, n, g_arr, ns))
+        self._pending.append((p, n, total_q))
+
+    def take(self, stream=None) -> Plan:
+        if not self._pending:
+            raise MStarError(ERR_INVALID_ARG, "no plan was submitted")
+        p, n, total_q = self._pending.pop(0)
+        h = ctypes.c_void_p(None)
+        stream_h = None if p.flags & FLAG_HOST_ONLY else _stream_handle(stream)
+        _check_rc(lib().mstar_planner_take(self._h, stream_h, ctypes.byref(h)))
+        return Plan(h.value, p, n, total_q)
+
+    def close(self):
+        if self._h:
+            lib().mstar_planner_destroy(self._h)
+            self._h = ctypes.c_void_p(None)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def _need(cond, msg):

@@ -5,9 +5,14 @@
 
 #include <algorithm>
 #include <chrono>
+#include <condition_variable>
 #include <cstring>
+#include <deque>
+#include <mutex>
 #include <new>
 #include <string>
+#include <thread>
+#include <vector>
 
 #include "mstar_attn.h"
 #include "kernels.h"
@@ -22,6 +27,7 @@ struct mstar_plan {
     size_t bytes = 0;
     size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_order = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_append = 0, off_err = 0;
     double plan_us = 0.0;
+    hipEvent_t ready = nullptr;  // recorded after the upload by the async planner
 };
 
 namespace {
@@ -343,9 +349,199 @@ MSTAR_EXPORT int mstar_attn_plan_tile_order(const mstar_plan_t* plan, int32_t* p
 
 MSTAR_EXPORT void mstar_attn_plan_destroy(mstar_plan_t* plan) {
     if (!plan) return;
+    if (plan->ready) (void)hipEventDestroy(plan->ready);
     if (plan->dev) (void)hipFree(plan->dev);
     if (plan->pinned) (void)hipHostFree(plan->pinned);
     delete plan;
 }
 
 MSTAR_EXPORT const char* mstar_last_error(void) { return g_err.c_str(); }
+
+// ---------------------------------------------------------------------------
+// Async planner: plans built in submission order on a worker thread that owns
+// a HIP stream for the uploads; at most `depth` plans submitted and not yet
+// taken (two: the plan the current step uses and the one being built for the
+// next step).
+// ---------------------------------------------------------------------------
+struct mstar_planner {
+    struct Job {
+        uint64_t id = 0;
+        mstar_attn_params p{};
+        std::vector<mstar_seq_desc> seqs;
+        std::vector<mstar_mask_spec> masks;
+        std::vector<mstar_segment> segs;
+        int device = 0;
+    };
+    struct Done {
+        uint64_t id = 0;
+        int rc = MSTAR_OK;
+        std::string err;
+        mstar_plan_t* plan = nullptr;
+    };
+    std::mutex mu;
+    std::condition_variable cv_work, cv_done, cv_space;
+    std::deque<Job> jobs;
+    std::deque<Done> done;
+    size_t depth = 2, outstanding = 0;
+    uint64_t next_id = 0, next_take = 0;
+    bool stop = false;
+    std::thread worker;
+    hipStream_t stream = nullptr;  // touched by the worker only (and by destroy after the join)
+    int stream_device = -1;
+
+    void run() {
+        for (;;) {
+            Job job;
+            {
+                std::unique_lock<std::mutex> lk(mu);
+                cv_work.wait(lk, [&] { return stop || !jobs.empty(); });
+                if (jobs.empty()) return;
+                job = std::move(jobs.front());
+                jobs.pop_front();
+            }
+            Done d;
+            d.id = job.id;
+            const bool host_only = (job.p.flags & MSTAR_FLAG_HOST_ONLY) != 0;
+            void* s = nullptr;
+            if (!host_only) {
+                hipError_t e = hipSetDevice(job.device);
+                if (e == hipSuccess && (!stream || stream_device != job.device)) {
+                    if (stream) (void)hipStreamDestroy(stream);
+                    stream = nullptr;
+                    e = hipStreamCreateWithFlags(&stream, hipStreamNonBlocking);
+                    stream_device = e == hipSuccess ? job.device : -1;
+                }
+                if (e != hipSuccess) {
+                    d.rc = MSTAR_ERR_HIP;
+                    d.err = std::string("async planner stream: ") + hipGetErrorString(e);
+                }
+                s = stream;
+            }
+            if (d.rc == MSTAR_OK) {
+                d.rc = mstar_attn_plan(&job.p, job.seqs.data(), job.masks.data(), (int32_t)job.seqs.size(),
+                                       job.segs.data(), (int32_t)job.segs.size(), s, &d.plan);
+                if (d.rc != MSTAR_OK) {
+                    d.err = mstar_last_error();
+                } else if (!host_only) {
+                    hipEvent_t ev = nullptr;
+                    hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+                    if (e == hipSuccess) e = hipEventRecord(ev, stream);
+                    if (e != hipSuccess) {
+                        if (ev) (void)hipEventDestroy(ev);
+                        mstar_attn_plan_destroy(d.plan);
+                        d.plan = nullptr;
+                        d.rc = MSTAR_ERR_HIP;
+                        d.err = std::string("async planner event: ") + hipGetErrorString(e);
+                    } else {
+                        d.plan->ready = ev;
+                    }
+                }
+            }
+            {
+                std::lock_guard<std::mutex> lk(mu);
+                done.push_back(std::move(d));
+            }
+            cv_done.notify_all();
+        }
+    }
+};
+
+MSTAR_EXPORT int mstar_planner_create(int32_t depth, mstar_planner_t** out) {
+    if (!out) return fail(MSTAR_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    if (depth < 1 || depth > 64) return fail(MSTAR_ERR_INVALID_ARG, "depth must be in [1, 64]");
+    mstar_planner* pl = new (std::nothrow) mstar_planner();
+    if (!pl) return fail(MSTAR_ERR_NOMEM, "host allocation failed");
+    pl->depth = (size_t)depth;
+    try {
+        pl->worker = std::thread([pl] { pl->run(); });
+    } catch (...) {
+        delete pl;
+        return fail(MSTAR_ERR_NOMEM, "cannot start the planner thread");
+    }
+    *out = pl;
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_planner_submit(mstar_planner_t* planner, const mstar_attn_params* params,
+                                      const mstar_seq_desc* seqs, const mstar_mask_spec* masks, int32_t num_seqs,
+                                      const mstar_segment* segments, int32_t num_segs) {
+    if (!planner || !params) return fail(MSTAR_ERR_INVALID_ARG, "planner or params is NULL");
+    if (num_seqs < 0 || num_segs < 0) return fail(MSTAR_ERR_INVALID_ARG, "negative count");
+    if ((num_seqs > 0 && (!seqs || !masks)) || (num_segs > 0 && !segments))
+        return fail(MSTAR_ERR_INVALID_ARG, "descriptor pointer is NULL");
+    mstar_planner::Job job;
+    try {
+        job.p = *params;
+        job.seqs.assign(seqs, seqs + num_seqs);
+        job.masks.assign(masks, masks + num_seqs);
+        job.segs.assign(segments, segments + num_segs);
+    } catch (const std::bad_alloc&) {
+        return fail(MSTAR_ERR_NOMEM, "host allocation failed");
+    }
+    if (!(job.p.flags & MSTAR_FLAG_HOST_ONLY)) {
+        hipError_t e = hipGetDevice(&job.device);
+        if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    }
+    {
+        std::unique_lock<std::mutex> lk(planner->mu);
+        planner->cv_space.wait(lk, [&] { return planner->outstanding < planner->depth; });
+        job.id = planner->next_id++;
+        planner->jobs.push_back(std::move(job));
+        ++planner->outstanding;
+    }
+    planner->cv_work.notify_one();
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_planner_take(mstar_planner_t* planner, void* stream, mstar_plan_t** out) {
+    if (!planner || !out) return fail(MSTAR_ERR_INVALID_ARG, "planner or out is NULL");
+    *out = nullptr;
+    mstar_planner::Done d;
+    {
+        std::unique_lock<std::mutex> lk(planner->mu);
+        if (planner->outstanding == 0) return fail(MSTAR_ERR_INVALID_ARG, "no plan was submitted");
+        const uint64_t want = planner->next_take;
+        planner->cv_done.wait(lk, [&] { return !planner->done.empty() && planner->done.front().id == want; });
+        d = std::move(planner->done.front());
+        planner->done.pop_front();
+        ++planner->next_take;
+        --planner->outstanding;
+    }
+    planner->cv_space.notify_one();
+    if (d.rc != MSTAR_OK) return fail(d.rc, d.err);
+    if (d.plan->ready && stream) {
+        hipError_t e = hipStreamWaitEvent(static_cast<hipStream_t>(stream), d.plan->ready, 0);
+        if (e != hipSuccess) {
+            mstar_attn_plan_destroy(d.plan);
+            return hip_fail(e, "hipStreamWaitEvent(plan upload)");
+        }
+    }
+    *out = d.plan;
+    return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_attn_plan_wait(const mstar_plan_t* plan, void* stream) {
+    if (!plan) return fail(MSTAR_ERR_INVALID_ARG, "plan is NULL");
+    if (!plan->ready) return MSTAR_OK;
+    hipError_t e = hipStreamWaitEvent(static_cast<hipStream_t>(stream), plan->ready, 0);
+    return e == hipSuccess ? MSTAR_OK : hip_fail(e, "hipStreamWaitEvent(plan upload)");
+}
+
+MSTAR_EXPORT void mstar_planner_destroy(mstar_planner_t* planner) {
+    if (!planner) return;
+    {
+        std::lock_guard<std::mutex> lk(planner->mu);
+        planner->stop = true;
+    }
+    planner->cv_work.notify_all();
+    if (planner->worker.joinable()) planner->worker.join();
+    for (auto& d : planner->done) mstar_attn_plan_destroy(d.plan);
+    if (planner->stream) {
+        int cur = 0;
+        const bool have = hipGetDevice(&cur) == hipSuccess;
+        if (hipSetDevice(planner->stream_device) == hipSuccess) (void)hipStreamDestroy(planner->stream);
+        if (have) (void)hipSetDevice(cur);
+    }
+    delete planner;
+}
