@@ -41,11 +41,12 @@ PEAK_HBM_GBS = 8000.0
 PEAK_BF16_TFLOPS = 2516.6   # dense MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
 PEAK_FP32_TFLOPS = 157.3
 BOUND = {"tiny_causal_f32": "alu", "decode_bf16": "hbm", "text_latent_bf16": "mfma",
-         "stream_window_bf16": "hbm", "rollout_bf16": "mfma", "cfg_labels_bf16": "mfma"}
-# kernel classes of mstar_attn_fwd_timed: 0 multi-row tiles, 1 few-row items, 2 fp32, 3 merge
-KERNEL_NAMES = ["tile_kernel", "few_kernel", "f32_kernel", "merge_kernel"]
+         "stream_window_bf16": "hbm", "rollout_bf16": "mfma", "cfg_labels_bf16": "mfma",
+         "shared_prefix_decode_bf16": "hbm"}
+# kernel classes of mstar_attn_fwd_timed: 0 multi-row tiles, 1 few-row items, 2 fp32, 3 merge, 4 cascade
+KERNEL_NAMES = ["tile_kernel", "few_kernel", "f32_kernel", "merge_kernel", "cascade_kernel"]
 DOMINANT = {"tiny_causal_f32": 2, "decode_bf16": 1, "text_latent_bf16": 0, "stream_window_bf16": 1,
-            "rollout_bf16": 0, "cfg_labels_bf16": 0}
+            "rollout_bf16": 0, "cfg_labels_bf16": 0, "shared_prefix_decode_bf16": 1}
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_12688_amd", "csrc", "kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -234,6 +235,9 @@ def main():
     ap.add_argument("--workload", default="decode_bf16", choices=sorted(BOUND))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cascade", action="store_true",
+                    help="plan with the workload's shared-prefix groups (mstar_attn_plan_cascade); the roofline "
+                         "then divides by the summed time of every kernel of the step")
     ap.add_argument("--op", default="attention", choices=["attention", "append", "serve"],
                     help="append: time mstar_kv_append (the step's new K/V rows into their pages); serve: a "
                          "serving loop that re-plans every step, planning inline vs on the async planner")
@@ -274,9 +278,14 @@ def main():
         return
     bound = BOUND[args.workload]
     stream = torch.cuda.current_stream()
+    if args.cascade and not b.prefix_groups:
+        print(f"{args.workload} declares no shared-prefix group", file=sys.stderr)
+        sys.exit(2)
+
     def make_plan():
         return attn.plan(b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, b.seqs, b.masks, b.segments,
-                         b.block_table.shape[1], b.num_pages, b.sm_scale, 0, stream)
+                         b.block_table.shape[1], b.num_pages, b.sm_scale, 0, stream,
+                         prefix_groups=b.prefix_groups if args.cascade else None)
     # the first plan of a process includes one-time set-up (pinned staging, HIP
     # context work); the reported planning time is that of a second plan
     pl_first = make_plan()
@@ -314,12 +323,14 @@ def main():
     # which would otherwise be charged to every step of a ~100 us workload
     K = args.steps
     launched = [k for k, n in enumerate(("prefill_items", "decode_items", "f32_items", "merge_rows")) if st[n] > 0]
+    if len(pl.items(4)):
+        launched.append(4)
     stride = max(1, K // 16)
     sampled = list(range(0, K, stride))
-    evs = {i: [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(2)] for i in sampled}
+    evs = {i: [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(2)] for i in sampled}
     ev_arrays = {}
     for i in sampled:
-        arr = [(ctypes.c_void_p * 4)(), (ctypes.c_void_p * 4)()]
+        arr = [(ctypes.c_void_p * 5)(), (ctypes.c_void_p * 5)()]
         for side in range(2):
             for k in launched:
                 evs[i][side][k].record(stream)  # creates the event
@@ -345,7 +356,12 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / K
     per_kernel = {KERNEL_NAMES[k]: np.array([evs[i][0][k].elapsed_time(evs[i][1][k]) for i in sampled])
                   for k in launched}
-    kernel_ms = per_kernel[KERNEL_NAMES[DOMINANT[args.workload]]]
+    if args.cascade:  # the step's work is spread over several kernels: their summed time
+        kernel_ms = sum(per_kernel.values())
+        dominant = "+".join(KERNEL_NAMES[k] for k in launched)
+    else:
+        kernel_ms = per_kernel[KERNEL_NAMES[DOMINANT[args.workload]]]
+        dominant = KERNEL_NAMES[DOMINANT[args.workload]]
     assert attn.check(pl, stream) == 0
 
     tflops = flop / (ms_per_step * 1e-3) / 1e12
@@ -380,7 +396,7 @@ def main():
                      "frac": round(achieved / peak, 4), "traffic": traffic},
         "tflops": round(tflops, 3), "kv_gbps": round(gbps, 3),
         "tflops_frac_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4), "kv_gbps_frac_hbm_peak": round(gbps / PEAK_HBM_GBS, 4),
-        "dominant_kernel": KERNEL_NAMES[DOMINANT[args.workload]],
+        "dominant_kernel": dominant, "cascade": bool(args.cascade),
         "kernel_ms": {name: {"mean": round(float(v.mean()), 5), "median": round(float(np.median(v)), 5),
                              "p95": round(float(np.percentile(v, 95)), 5)} for name, v in per_kernel.items()},
         "useful_flop": flop, "kv_bytes": nbytes, "plan_host_us": round(st["plan_host_us"], 1),

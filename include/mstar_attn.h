@@ -66,6 +66,8 @@ extern "C" {
 #define MSTAR_FLAG_HOST_ONLY 4u   /* plan on the host only: no device allocation or upload; for
                                      inspection (stats, items, key ranges) without a GPU; fwd
                                      rejects such a plan                                         */
+#define MSTAR_FLAG_CASCADE_ALL 8u /* mstar_attn_plan_cascade: every group member joins the cascade,
+                                     not only the decode-like ones                               */
 
 /* Bits of the sticky device error word (see mstar_attn_check). */
 #define MSTAR_DEVERR_PAGE_RANGE 1 /* a block-table entry was outside [0, num_pages) */
@@ -110,6 +112,20 @@ typedef struct {
     float sm_scale;             /* score scale > 0, typically 1/sqrt(head_dim)    */
 } mstar_attn_params;
 
+/* A shared-prefix group (for mstar_attn_plan_cascade): the requests listed
+ * in members[member_begin .. member_begin + member_count) of the member array
+ * keep their first prefix_len keys (a positive multiple of 16) in the same
+ * physical pages -- their block tables agree on the first prefix_len / 16
+ * entries -- and every query row of each of them sees all of those keys.
+ * Candidates of one batched forward over a shared context (App. A, V-JEPA 2
+ * MPC Walk), or contexts stored as labels over one pool with a common prefix
+ * (Sec. 4.1), are such groups. */
+typedef struct {
+    int32_t member_begin;
+    int32_t member_count;
+    int32_t prefix_len;
+} mstar_prefix_group;
+
 typedef struct mstar_plan mstar_plan_t;
 typedef struct mstar_planner mstar_planner_t;
 
@@ -147,6 +163,28 @@ int mstar_attn_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                     const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segments,
                     int32_t num_segs, void* upload_stream, mstar_plan_t** out);
 
+/* mstar_attn_plan with shared-prefix groups (a cascade).  For each group the
+ * prefix keys are attended once for the query rows of all members together
+ * -- 128 rows (member, query row, query head) per tile against one copy of
+ * each prefix K/V tile, read through the first member's block table -- and
+ * each member's own keys [prefix_len, ...) separately; the two partial
+ * results of every (row, head) are combined by their log-sum-exps.  Results
+ * equal those of mstar_attn_plan up to rounding.  Only decode-like members
+ * (query rows x (Hq / Hkv) <= 64, which mstar_attn_plan gives to the few-row
+ * kernel, one pass over all of their keys per KV head) join the cascade: a
+ * member with more rows already reads each prefix tile once per 128 rows, so
+ * the cascade would only add the merge; such members are planned as by
+ * mstar_attn_plan, unless MSTAR_FLAG_CASCADE_ALL is set.  A request may belong to at
+ * most one group.  Errors as mstar_attn_plan, plus INVALID_ARG for a bad group
+ * (member index out of range or repeated, prefix_len not a positive multiple
+ * of 16 or longer than a member's kv_len, or a member query row that does not
+ * see every prefix key) and UNSUPPORTED for the fp32 dtype.  The plan needs
+ * a workspace (mstar_attn_workspace_bytes).  num_groups = 0 is mstar_attn_plan. */
+int mstar_attn_plan_cascade(const mstar_attn_params* params, const mstar_seq_desc* seqs,
+                            const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segments,
+                            int32_t num_segs, const mstar_prefix_group* groups, int32_t num_groups,
+                            const int32_t* members, int32_t num_members, void* upload_stream, mstar_plan_t** out);
+
 /* Bytes of device scratch fwd needs (fp32 partial outputs and their LSEs for
  * split key ranges); 0 if nothing is split.  Returns 0 for a NULL plan. */
 size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan);
@@ -173,7 +211,8 @@ int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const void* k_pages,
 /* mstar_attn_fwd, additionally recording caller-created HIP events
  * (hipEvent_t) on `stream` right before and right after each kernel it
  * enqueues: index 0 = multi-row tile kernel, 1 = few-row kernel, 2 = fp32
- * kernel, 3 = merge kernel.  Either array, and any entry, may be NULL; events
+ * kernel, 3 = merge kernel, 4 = shared-prefix cascade kernel (arrays of 5
+ * entries).  Either array, and any entry, may be NULL; events
  * of kernels the plan does not launch are left untouched.  For per-kernel
  * timing (profiling); same contract and errors as mstar_attn_fwd. */
 int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, const void* k_pages,
@@ -194,24 +233,39 @@ int mstar_attn_plan_stats(const mstar_plan_t* plan, mstar_plan_stats* out);
 int mstar_attn_plan_key_ranges(const mstar_plan_t* plan, int32_t* lo_hi, int32_t num_seqs);
 
 /* Copy one host-side list of the plan (0 = multi-row tiles, 1 = few-row
- * items, 2 = fp32 items, 3 = rows merged by the merge kernel) into `items` as
- * int32 records of 8 fields; *count receives the number of records, and at
- * most `capacity` records are written.  For inspection and tests.
- * Work record: seq, head (query head; KV head for class 1; -1 for class 0,
- *              whose records serve every query head), row0, nrows, key_begin,
- *              key_end, partial_slot (-1 = final), head_stride (class 0 with a
- *              split key range: query head h, row r writes partial slot
- *              partial_slot + h * head_stride + r; otherwise -1).
- * Merge record: packed_row, head, slot0, slot_stride, nslots, 0, 0, 0. */
+ * items, 2 = fp32 items, 3 = rows merged by the merge kernel, 4 = cascade
+ * items, 5 = cascade rows) into `items` as int32 records of 8 fields; *count
+ * receives the number of records, and at most `capacity` records are written.
+ * For inspection and tests.
+ * Work record: seq, head (query head; KV head for classes 1 and 4; -1 for
+ *              class 0, whose records serve every query head), row0, nrows,
+ *              key_begin, key_end, partial_slot (-1 = final), head_stride
+ *              (class 0 with a split key range or a cascade member: query head
+ *              h, row r writes partial slot partial_slot + h * head_stride + r;
+ *              otherwise -1).  A cascade item (class 4) reads keys through the
+ *              block table of request `seq`, its rows are entries row0 ..
+ *              row0 + nrows - 1 of the cascade rows, and row r writes partial
+ *              slot partial_slot + r.
+ * Merge record: packed_row, head, slot0, slot_stride, nslots, prefix_slot0,
+ *              prefix_stride, prefix_nslots (the output combines the partials
+ *              at slot0 + s * slot_stride, s < nslots, and at prefix_slot0 +
+ *              s * prefix_stride, s < prefix_nslots).
+ * Cascade row record: packed query row, query head, 0, 0, 0, 0, 0, 0. */
 int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, int32_t* items,
                           int64_t capacity, int64_t* count);
 
 /* Launch order of the multi-row kernel: *count receives the number of
  * workgroups (a multiple of 8) and at most `capacity` (tile item, query head)
  * int32 pairs are written to pairs[2*capacity]; (-1, -1) marks a padding
- * workgroup.  Workgroup b runs on XCD b % 8; all workgroups that read one
- * request's pages for one KV head share an XCD.  For inspection and tests. */
+ * workgroup.  Workgroup b runs on XCD b % 8; the workgroups that read one
+ * request's pages for one KV head run consecutively on one XCD, except that a
+ * request whose work exceeds an eighth of the launch is cut into runs of
+ * consecutive items spread over several XCDs.  For inspection and tests. */
 int mstar_attn_plan_tile_order(const mstar_plan_t* plan, int32_t* pairs, int64_t capacity, int64_t* count);
+
+/* The same for the cascade kernel: (cascade item, a query head of its KV
+ * head) pairs; empty for a plan without cascade items. */
+int mstar_attn_plan_cascade_order(const mstar_plan_t* plan, int32_t* pairs, int64_t capacity, int64_t* count);
 
 /* Asynchronous, double-buffered planning.  The paper's workers build the
  * attention plan of the next batch on a separate thread and stream while the

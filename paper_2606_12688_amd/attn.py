@@ -30,11 +30,12 @@ ERR_NOMEM = -5
 
 SEG_CAUSAL, SEG_FULL, SEG_BLOCKS = 0, 1, 2
 DTYPE_F32, DTYPE_BF16 = 0, 1
-FLAG_FORCE_SPLIT, FLAG_NO_SPLIT, FLAG_HOST_ONLY = 1, 2, 4
+FLAG_FORCE_SPLIT, FLAG_NO_SPLIT, FLAG_HOST_ONLY, FLAG_CASCADE_ALL = 1, 2, 4, 8
 DEVERR_PAGE_RANGE = 1
 
 EXPORTS = [
     "mstar_attn_plan",
+    "mstar_attn_plan_cascade",
     "mstar_attn_workspace_bytes",
     "mstar_attn_fwd",
     "mstar_attn_fwd_timed",
@@ -43,6 +44,7 @@ EXPORTS = [
     "mstar_attn_plan_key_ranges",
     "mstar_attn_plan_items",
     "mstar_attn_plan_tile_order",
+    "mstar_attn_plan_cascade_order",
     "mstar_kv_append",
     "mstar_planner_create",
     "mstar_planner_submit",
@@ -61,6 +63,10 @@ class Segment(ctypes.Structure):
 
 class MaskSpec(ctypes.Structure):
     _fields_ = [("seg_begin", ctypes.c_int32), ("seg_count", ctypes.c_int32), ("window", ctypes.c_int32)]
+
+
+class PrefixGroup(ctypes.Structure):
+    _fields_ = [("member_begin", ctypes.c_int32), ("member_count", ctypes.c_int32), ("prefix_len", ctypes.c_int32)]
 
 
 class SeqDesc(ctypes.Structure):
@@ -102,6 +108,10 @@ def lib() -> ctypes.CDLL:
     L.mstar_attn_plan.argtypes = [ctypes.POINTER(Params), ctypes.POINTER(SeqDesc), ctypes.POINTER(MaskSpec), i32,
                                   ctypes.POINTER(Segment), i32, vp, ctypes.POINTER(vp)]
     L.mstar_attn_plan.restype = ctypes.c_int
+    L.mstar_attn_plan_cascade.argtypes = [ctypes.POINTER(Params), ctypes.POINTER(SeqDesc), ctypes.POINTER(MaskSpec),
+                                          i32, ctypes.POINTER(Segment), i32, ctypes.POINTER(PrefixGroup), i32,
+                                          ctypes.POINTER(i32), i32, vp, ctypes.POINTER(vp)]
+    L.mstar_attn_plan_cascade.restype = ctypes.c_int
     L.mstar_attn_workspace_bytes.argtypes = [vp]
     L.mstar_attn_workspace_bytes.restype = sz
     L.mstar_attn_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -118,6 +128,8 @@ def lib() -> ctypes.CDLL:
     L.mstar_attn_plan_items.restype = ctypes.c_int
     L.mstar_attn_plan_tile_order.argtypes = [vp, vp, i64, ctypes.POINTER(i64)]
     L.mstar_attn_plan_tile_order.restype = ctypes.c_int
+    L.mstar_attn_plan_cascade_order.argtypes = [vp, vp, i64, ctypes.POINTER(i64)]
+    L.mstar_attn_plan_cascade_order.restype = ctypes.c_int
     L.mstar_kv_append.argtypes = [vp, vp, vp, vp, vp, vp, vp]
     L.mstar_kv_append.restype = ctypes.c_int
     L.mstar_planner_create.argtypes = [i32, ctypes.POINTER(vp)]
@@ -206,13 +218,15 @@ class Plan:
         _check_rc(lib().mstar_attn_plan_items(self.handle, kind, out.ctypes.data, cnt.value, ctypes.byref(cnt)))
         return out[: cnt.value]
 
-    def tile_order(self) -> np.ndarray:
+    def tile_order(self, cascade: bool = False) -> np.ndarray:
         """(tile item, query head) of every multi-row workgroup in launch order, as an int32 [n, 2] array
-        (``mstar_attn_plan_tile_order``); (-1, -1) marks padding."""
+        (``mstar_attn_plan_tile_order``, or ``mstar_attn_plan_cascade_order`` for the cascade kernel);
+        (-1, -1) marks padding."""
+        fn = lib().mstar_attn_plan_cascade_order if cascade else lib().mstar_attn_plan_tile_order
         cnt = ctypes.c_int64(0)
-        _check_rc(lib().mstar_attn_plan_tile_order(self.handle, None, 0, ctypes.byref(cnt)))
+        _check_rc(fn(self.handle, None, 0, ctypes.byref(cnt)))
         out = np.zeros((cnt.value, 2), dtype=np.int32)
-        _check_rc(lib().mstar_attn_plan_tile_order(self.handle, out.ctypes.data, cnt.value, ctypes.byref(cnt)))
+        _check_rc(fn(self.handle, out.ctypes.data, cnt.value, ctypes.byref(cnt)))
         return out
 
     def destroy(self):
@@ -246,15 +260,29 @@ def _descriptors(num_qo_heads, num_kv_heads, head_dim, dtype, seqs, masks, segme
 
 def plan(num_qo_heads: int, num_kv_heads: int, head_dim: int, dtype: str, seqs, masks, segments,
          max_blocks_per_seq: int, num_pages: int, sm_scale: Optional[float] = None, flags: int = 0,
-         stream=None, page_size: int = 16) -> Plan:
+         stream=None, page_size: int = 16, prefix_groups=None) -> Plan:
     """``mstar_attn_plan``: ``seqs [n,3]`` (q_len, kv_len, q_start), ``masks [n,3]``
-    (seg_begin, seg_count, window), ``segments [S,4]`` (start, len, kind, block)."""
+    (seg_begin, seg_count, window), ``segments [S,4]`` (start, len, kind, block).
+    With ``prefix_groups`` (``[(member request indices, prefix_len), ...]``),
+    ``mstar_attn_plan_cascade``."""
     p, s_arr, n, m_arr, g_arr, ns, total_q = _descriptors(num_qo_heads, num_kv_heads, head_dim, dtype, seqs, masks,
                                                           segments, max_blocks_per_seq, num_pages, sm_scale,
                                                           flags, page_size)
     h = ctypes.c_void_p(None)
     stream_h = None if flags & FLAG_HOST_ONLY else _stream_handle(stream)
-    _check_rc(lib().mstar_attn_plan(ctypes.byref(p), s_arr, m_arr, n, g_arr, ns, stream_h, ctypes.byref(h)))
+    if prefix_groups:
+        # prefix_groups: [(member request indices, prefix_len), ...]
+        members = [int(r) for mem, _ in prefix_groups for r in mem]
+        gr = (PrefixGroup * len(prefix_groups))()
+        k = 0
+        for i, (mem, plen) in enumerate(prefix_groups):
+            gr[i].member_begin, gr[i].member_count, gr[i].prefix_len = k, len(mem), int(plen)
+            k += len(mem)
+        mem_arr = (ctypes.c_int32 * max(len(members), 1))(*members)
+        _check_rc(lib().mstar_attn_plan_cascade(ctypes.byref(p), s_arr, m_arr, n, g_arr, ns, gr, len(prefix_groups),
+                                                mem_arr, len(members), stream_h, ctypes.byref(h)))
+    else:
+        _check_rc(lib().mstar_attn_plan(ctypes.byref(p), s_arr, m_arr, n, g_arr, ns, stream_h, ctypes.byref(h)))
     return Plan(h.value, p, n, total_q)
 
 

@@ -25,7 +25,7 @@ struct mstar_plan {
     void* dev = nullptr;     // device copy of the plan blob
     void* pinned = nullptr;  // pinned staging copy (kept until destroy)
     size_t bytes = 0;
-    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_order = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_append = 0, off_err = 0;
+    size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_order = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_append = 0, off_casc = 0, off_casc_rows = 0, off_casc_order = 0, off_err = 0;
     double plan_us = 0.0;
     hipEvent_t ready = nullptr;  // recorded after the upload by the async planner
 };
@@ -55,10 +55,10 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 }  // namespace
 
-MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
-                                 const mstar_mask_spec* masks, int32_t num_seqs,
-                                 const mstar_segment* segments, int32_t num_segs, void* upload_stream,
-                                 mstar_plan_t** out) {
+static int plan_impl(const mstar_attn_params* params, const mstar_seq_desc* seqs, const mstar_mask_spec* masks,
+                     int32_t num_seqs, const mstar_segment* segments, int32_t num_segs,
+                     const mstar_prefix_group* groups, int32_t num_groups, const int32_t* members,
+                     int32_t num_members, void* upload_stream, mstar_plan_t** out) {
     const auto t0 = std::chrono::steady_clock::now();
     if (!out) return fail(MSTAR_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
@@ -72,7 +72,8 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     std::string err;
     int rc;
     try {
-        rc = mstar::build_host_plan(&p, seqs, masks, num_seqs, segments, num_segs, plan->host, err);
+        rc = mstar::build_host_plan(&p, seqs, masks, num_seqs, segments, num_segs, plan->host, err, groups,
+                                    num_groups, members, num_members);
     } catch (const std::bad_alloc&) {
         rc = MSTAR_ERR_NOMEM;
         err = "host allocation failed";
@@ -86,7 +87,7 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     }
     const mstar::HostPlan& h = plan->host;
 
-    // blob layout: seqs | row_hi | tiles | tile order | few | f32 | merges | appends | error word
+    // blob layout: seqs | row_hi | tiles | tile order | few | f32 | merges | appends | cascade items, rows, order | error word
     size_t off = 0;
     plan->off_seqs = off;   off = align256(off + h.seqs.size() * sizeof(mstar::SeqInfo));
     plan->off_row_hi = off; off = align256(off + h.row_hi.size() * sizeof(int32_t));
@@ -96,6 +97,9 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     plan->off_f32 = off;    off = align256(off + h.f32.size() * sizeof(mstar::WorkItem));
     plan->off_merge = off;  off = align256(off + h.merges.size() * sizeof(mstar::MergeItem));
     plan->off_append = off; off = align256(off + h.appends.size() * sizeof(mstar::WorkItem));
+    plan->off_casc = off;   off = align256(off + h.cascade.size() * sizeof(mstar::WorkItem));
+    plan->off_casc_rows = off; off = align256(off + h.casc_rows.size() * sizeof(int32_t));
+    plan->off_casc_order = off; off = align256(off + h.casc_order.size() * sizeof(int32_t));
     plan->off_err = off;    off = align256(off + sizeof(int32_t));
     plan->bytes = off;
 
@@ -115,6 +119,9 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
         put(blob, plan->off_f32, h.f32);
         put(blob, plan->off_merge, h.merges);
         put(blob, plan->off_append, h.appends);
+        put(blob, plan->off_casc, h.cascade);
+        put(blob, plan->off_casc_rows, h.casc_rows);
+        put(blob, plan->off_casc_order, h.casc_order);
         e = hipMalloc(&plan->dev, plan->bytes);
         if (e != hipSuccess) {
             (void)hipHostFree(plan->pinned);
@@ -133,6 +140,23 @@ MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_se
     plan->plan_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
     *out = plan;
     return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
+                                 const mstar_mask_spec* masks, int32_t num_seqs,
+                                 const mstar_segment* segments, int32_t num_segs, void* upload_stream,
+                                 mstar_plan_t** out) {
+    return plan_impl(params, seqs, masks, num_seqs, segments, num_segs, nullptr, 0, nullptr, 0, upload_stream, out);
+}
+
+MSTAR_EXPORT int mstar_attn_plan_cascade(const mstar_attn_params* params, const mstar_seq_desc* seqs,
+                                         const mstar_mask_spec* masks, int32_t num_seqs,
+                                         const mstar_segment* segments, int32_t num_segs,
+                                         const mstar_prefix_group* groups, int32_t num_groups,
+                                         const int32_t* members, int32_t num_members, void* upload_stream,
+                                         mstar_plan_t** out) {
+    return plan_impl(params, seqs, masks, num_seqs, segments, num_segs, groups, num_groups, members, num_members,
+                     upload_stream, out);
 }
 
 MSTAR_EXPORT size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan) {
@@ -155,7 +179,7 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
     if (!plan) return fail(MSTAR_ERR_INVALID_ARG, "plan is NULL");
     if (!plan->dev) return fail(MSTAR_ERR_INVALID_ARG, "plan was built host-only");
     const mstar::HostPlan& h = plan->host;
-    const bool any_work = !h.tiles.empty() || !h.few.empty() || !h.f32.empty();
+    const bool any_work = !h.tiles.empty() || !h.few.empty() || !h.f32.empty() || !h.cascade.empty();
     if (!any_work) return MSTAR_OK;
     if (!q || !k_pages || !v_pages || !block_table || !out || !lse)
         return fail(MSTAR_ERR_INVALID_ARG, "a tensor pointer is NULL");
@@ -192,7 +216,7 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
     hipStream_t s = static_cast<hipStream_t>(stream);
 
     hipError_t e;
-    // optional HIP events around kernel class k (0 tiles, 1 few-row, 2 fp32, 3 merge)
+    // optional HIP events around kernel class k (0 tiles, 1 few-row, 2 fp32, 3 merge, 4 cascade)
     auto mark = [&](void* const* evs, int k) -> hipError_t {
         if (!evs || !evs[k]) return hipSuccess;
         return hipEventRecord(static_cast<hipEvent_t>(evs[k]), s);
@@ -207,6 +231,16 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
         MSTAR_MARK(events_before, 0);
         if ((e = mstar::launch_tiles(a, D, s)) != hipSuccess) return hip_fail(e, "tile kernel launch");
         MSTAR_MARK(events_after, 0);
+    }
+    if (!h.cascade.empty()) {
+        a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_casc);
+        a.n_items = (int32_t)h.cascade.size();
+        a.order = reinterpret_cast<const int32_t*>(blob + plan->off_casc_order);
+        a.n_wgs = (int32_t)(h.casc_order.size() / 2);
+        a.rows = reinterpret_cast<const int32_t*>(blob + plan->off_casc_rows);
+        MSTAR_MARK(events_before, 4);
+        if ((e = mstar::launch_cascade(a, D, s)) != hipSuccess) return hip_fail(e, "cascade kernel launch");
+        MSTAR_MARK(events_after, 4);
     }
     if (!h.few.empty()) {
         a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_few);
@@ -327,7 +361,20 @@ MSTAR_EXPORT int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, i
         case 1: src = h.few.data(); n = h.few.size(); break;
         case 2: src = h.f32.data(); n = h.f32.size(); break;
         case 3: src = h.merges.data(); n = h.merges.size(); break;
-        default: return fail(MSTAR_ERR_INVALID_ARG, "kind must be 0..3");
+        case 4: src = h.cascade.data(); n = h.cascade.size(); break;
+        case 5: {  // cascade rows, one (packed query row, query head, 0, ..., 0) record each
+            n = h.casc_rows.size() / 2;
+            *count = (int64_t)n;
+            if (capacity > 0 && !items) return fail(MSTAR_ERR_INVALID_ARG, "items is NULL");
+            const size_t m = capacity < 0 ? 0 : std::min<size_t>(n, (size_t)capacity);
+            for (size_t i = 0; i < m; ++i) {
+                std::memset(items + 8 * i, 0, 32);
+                items[8 * i] = h.casc_rows[2 * i];
+                items[8 * i + 1] = h.casc_rows[2 * i + 1];
+            }
+            return MSTAR_OK;
+        }
+        default: return fail(MSTAR_ERR_INVALID_ARG, "kind must be 0..5");
     }
     *count = (int64_t)n;
     if (capacity > 0 && !items) return fail(MSTAR_ERR_INVALID_ARG, "items is NULL");
@@ -336,15 +383,24 @@ MSTAR_EXPORT int mstar_attn_plan_items(const mstar_plan_t* plan, int32_t kind, i
     return MSTAR_OK;
 }
 
-MSTAR_EXPORT int mstar_attn_plan_tile_order(const mstar_plan_t* plan, int32_t* pairs, int64_t capacity,
-                                            int64_t* count) {
-    if (!plan || !count) return fail(MSTAR_ERR_INVALID_ARG, "plan or count is NULL");
-    const std::vector<int32_t>& o = plan->host.tile_order;
+static int copy_order(const std::vector<int32_t>& o, int32_t* pairs, int64_t capacity, int64_t* count) {
     *count = (int64_t)(o.size() / 2);
     if (capacity > 0 && !pairs) return fail(MSTAR_ERR_INVALID_ARG, "pairs is NULL");
     const size_t m = capacity < 0 ? 0 : std::min<size_t>(o.size() / 2, (size_t)capacity);
     if (m) std::memcpy(pairs, o.data(), m * 2 * sizeof(int32_t));
     return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_attn_plan_tile_order(const mstar_plan_t* plan, int32_t* pairs, int64_t capacity,
+                                            int64_t* count) {
+    if (!plan || !count) return fail(MSTAR_ERR_INVALID_ARG, "plan or count is NULL");
+    return copy_order(plan->host.tile_order, pairs, capacity, count);
+}
+
+MSTAR_EXPORT int mstar_attn_plan_cascade_order(const mstar_plan_t* plan, int32_t* pairs, int64_t capacity,
+                                               int64_t* count) {
+    if (!plan || !count) return fail(MSTAR_ERR_INVALID_ARG, "plan or count is NULL");
+    return copy_order(plan->host.casc_order, pairs, capacity, count);
 }
 
 MSTAR_EXPORT void mstar_attn_plan_destroy(mstar_plan_t* plan) {

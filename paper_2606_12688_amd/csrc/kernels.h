@@ -12,6 +12,7 @@ struct KArgs {
     const int32_t* row_hi;
     const WorkItem* items;
     const int32_t* order;  // multi-row launch: (item, query head) per workgroup
+    const int32_t* rows;   // cascade launch: (packed query row, query head) of every row
     const void* q;
     const void* k;
     const void* v;
@@ -53,6 +54,7 @@ struct AArgs {
 };
 
 hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_cascade(const KArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_append(const AArgs& a, hipStream_t s);
 hipError_t launch_few(const KArgs& a, int head_dim, int row_blocks, hipStream_t s);
 hipError_t launch_f32(const KArgs& a, int head_dim, hipStream_t s);

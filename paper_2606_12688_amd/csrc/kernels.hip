@@ -311,7 +311,7 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
 // valid offset in range and pushes the marker offset below out of range.
 constexpr uint32_t kSmallPoolBytes = 0x80000000u;
 
-template <int D, int RBW, bool SMALL>
+template <int D, int RBW, bool SMALL, bool CASC>
 __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
     constexpr int BN = kTileKeys;
     constexpr int RBY = 2 * D;       // bytes per K/V row in LDS
@@ -345,6 +345,9 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
     const RowGroup rg;
 
     // ---- rows owned by this lane ------------------------------------------
+    // CASC (a shared-prefix cascade item): row r is entry row0 + r of the row
+    // list, a (packed query row, query head) of some group member; every key
+    // of the item is visible to it.
     int32_t lo[RBW], hi[RBW];
     bool valid[RBW];
     bf16x8 qf[RBW][DS];
@@ -354,8 +357,15 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
         valid[rb] = r < it.nrows;
         lo[rb] = 0;
         hi[rb] = 0;
-        if (valid[rb]) row_interval(a, si, it, it.row0 + r, lo[rb], hi[rb]);
-        const int64_t qoff = ((int64_t)(si.q_start + it.row0 + r) * a.hq + head) * D;
+        int64_t qoff;
+        if constexpr (CASC) {
+            if (valid[rb]) hi[rb] = it.k_end;
+            const int32_t e = valid[rb] ? it.row0 + r : it.row0;
+            qoff = ((int64_t)a.rows[2 * e] * a.hq + a.rows[2 * e + 1]) * D;
+        } else {
+            if (valid[rb]) row_interval(a, si, it, it.row0 + r, lo[rb], hi[rb]);
+            qoff = ((int64_t)(si.q_start + it.row0 + r) * a.hq + head) * D;
+        }
 #pragma unroll
         for (int s = 0; s < DS; ++s) {
             if (valid[rb]) {
@@ -372,8 +382,12 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
     const bool wave_active = wr0 < it.nrows;
     int32_t w_lo_min = 0, w_lo_max = 0, w_hi_min = 0, w_hi_max = 0;
     if (wave_active) {
-        row_interval(a, si, it, it.row0 + wr0, w_lo_min, w_hi_min);
-        row_interval(a, si, it, it.row0 + wr1, w_lo_max, w_hi_max);
+        if constexpr (CASC) {
+            w_hi_min = w_hi_max = it.k_end;  // lo = 0 for every row
+        } else {
+            row_interval(a, si, it, it.row0 + wr0, w_lo_min, w_hi_min);
+            row_interval(a, si, it, it.row0 + wr1, w_lo_max, w_hi_max);
+        }
     }
 
     float m[RBW], l[RBW];
@@ -598,7 +612,14 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
         const int r = wave * 16 * RBW + rb * 16 + n;
         const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
         const float lse = lt > 0.0f ? (m[rb] + __log2f(lt)) * kLn2 : kNegInf;
-        if (it.part < 0) {
+        if constexpr (CASC) {
+            const int64_t slot = it.part + r;  // cascade items always write partials
+            float* po = a.part_o + slot * D;
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+                *reinterpret_cast<f32x4*>(po + db * 16 + 4 * grp) = o[rb][db] * inv;
+            if (grp == 0) a.part_lse[slot] = lse;
+        } else if (it.part < 0) {
             const int64_t row = (int64_t)(si.q_start + it.row0 + r) * a.hq + head;
             bf16_t* out = reinterpret_cast<bf16_t*>(a.out) + row * D;
 #pragma unroll
@@ -1016,7 +1037,8 @@ __global__ __launch_bounds__(256) void f32_kernel(KArgs a) {
 
 // ---------------------------------------------------------------------------
 // Merge kernel: one wave per (row, head); combines the partial results of
-// split key ranges by their log-sum-exps (lanes over the head dimension).
+// split key ranges (and of a shared prefix, for cascade members) by their
+// log-sum-exps (lanes over the head dimension).
 // ---------------------------------------------------------------------------
 template <int D, bool BF16>
 __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
@@ -1025,18 +1047,55 @@ __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
     const int lane = threadIdx.x & 63;
     if (idx >= a.n_items) return;
     const MergeItem mi = a.items[idx];
+    // slot set 1: slot0 + s * stride, s < nslots (split key ranges of the row's
+    // own keys); slot set 2: pad0 + s * pad1, s < pad2 (the chunks of a shared
+    // prefix, for cascade members; empty otherwise)
+    auto slot_of = [&](int s) -> int64_t {
+        return s < mi.nslots ? mi.slot0 + (int64_t)s * mi.stride : mi.pad0 + (int64_t)(s - mi.nslots) * mi.pad1;
+    };
+    const int n = mi.nslots + mi.pad2;
+    // the slots' LSEs are read across the lanes, 64 at a time, and reduced
+    // over the wave (a fixed order: the result does not depend on timing)
     float mstar = kNegInf;
-    for (int s = 0; s < mi.nslots; ++s) mstar = fmaxf(mstar, a.part_lse[mi.slot0 + (int64_t)s * mi.stride]);
+    for (int s0 = 0; s0 < n; s0 += 64) {
+        float x = s0 + lane < n ? a.part_lse[slot_of(s0 + lane)] : kNegInf;
+        for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
+        mstar = fmaxf(mstar, x);
+    }
     float acc[E], tot = 0.0f;
 #pragma unroll
     for (int e = 0; e < E; ++e) acc[e] = 0.0f;
     if (mstar != kNegInf) {
-        for (int s = 0; s < mi.nslots; ++s) {
-            const int64_t slot = mi.slot0 + (int64_t)s * mi.stride;
-            const float w = expf(a.part_lse[slot] - mstar);
-            tot += w;
+        for (int s0 = 0; s0 < n; s0 += 64) {
+            const int cnt = min(64, n - s0);
+            // lane j holds the weight of slot s0 + j
+            float w = lane < cnt ? expf(a.part_lse[slot_of(s0 + lane)] - mstar) : 0.0f;
+            float ws = w;
+            for (int off = 32; off > 0; off >>= 1) ws += __shfl_xor(ws, off, 64);
+            tot += ws;
+            // four slots' rows loaded together, then accumulated in slot order
+            int j = 0;
+            for (; j + 4 <= cnt; j += 4) {
+                float v[4][E];
 #pragma unroll
-            for (int e = 0; e < E; ++e) acc[e] = fmaf(w, a.part_o[slot * D + lane + 64 * e], acc[e]);
+                for (int u = 0; u < 4; ++u) {
+                    const int64_t slot = slot_of(s0 + j + u);
+#pragma unroll
+                    for (int e = 0; e < E; ++e) v[u][e] = a.part_o[slot * D + lane + 64 * e];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const float wj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), j + u));
+#pragma unroll
+                    for (int e = 0; e < E; ++e) acc[e] = fmaf(wj, v[u][e], acc[e]);
+                }
+            }
+            for (; j < cnt; ++j) {
+                const int64_t slot = slot_of(s0 + j);
+                const float wj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), j));
+#pragma unroll
+                for (int e = 0; e < E; ++e) acc[e] = fmaf(wj, a.part_o[slot * D + lane + 64 * e], acc[e]);
+            }
         }
     }
     const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
@@ -1104,11 +1163,26 @@ hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s) {
     const uint64_t pool_bytes = (uint64_t)a.num_pages * 16 * a.hkv * head_dim * 2;
     const bool small = pool_bytes <= kSmallPoolBytes;
     if (head_dim == 64) {
-        if (small) hipLaunchKernelGGL((tile_kernel<64, 2, true>), g, b, 0, s, a);
-        else hipLaunchKernelGGL((tile_kernel<64, 2, false>), g, b, 0, s, a);
+        if (small) hipLaunchKernelGGL((tile_kernel<64, 2, true, false>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((tile_kernel<64, 2, false, false>), g, b, 0, s, a);
     } else {
-        if (small) hipLaunchKernelGGL((tile_kernel<128, 2, true>), g, b, 0, s, a);
-        else hipLaunchKernelGGL((tile_kernel<128, 2, false>), g, b, 0, s, a);
+        if (small) hipLaunchKernelGGL((tile_kernel<128, 2, true, false>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((tile_kernel<128, 2, false, false>), g, b, 0, s, a);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_cascade(const KArgs& a, int head_dim, hipStream_t s) {
+    if (a.n_items == 0) return hipSuccess;
+    const dim3 g((unsigned)a.n_wgs), b(256);
+    const uint64_t pool_bytes = (uint64_t)a.num_pages * 16 * a.hkv * head_dim * 2;
+    const bool small = pool_bytes <= kSmallPoolBytes;
+    if (head_dim == 64) {
+        if (small) hipLaunchKernelGGL((tile_kernel<64, 2, true, true>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((tile_kernel<64, 2, false, true>), g, b, 0, s, a);
+    } else {
+        if (small) hipLaunchKernelGGL((tile_kernel<128, 2, true, true>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((tile_kernel<128, 2, false, true>), g, b, 0, s, a);
     }
     return hipGetLastError();
 }

@@ -38,7 +38,8 @@ struct WorkItem {
 };
 
 // Output (packed_row, head) assembled from nslots partials at
-// slot0 + s * stride.
+// slot0 + s * stride and pad2 partials at pad0 + s * pad1 (the chunks of a
+// shared prefix, for cascade members; pad2 = 0 otherwise).
 struct MergeItem {
     int32_t row, head, slot0, stride;
     int32_t nslots, pad0, pad1, pad2;

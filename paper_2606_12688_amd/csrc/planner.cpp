@@ -131,13 +131,15 @@ int32_t align_down16(int32_t x) { return x & ~(kPage - 1); }
 struct Unit {  // a few-row unit or a tile before key splitting
     int32_t seq, head, row0, nrows, k_begin, k_end;
     int64_t cost;
+    bool partial = false;  // write partials even when the key range is not split (cascade members)
 };
 
 }  // namespace
 
 int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                     const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segs,
-                    int32_t num_segs, HostPlan& plan, std::string& err) {
+                    int32_t num_segs, HostPlan& plan, std::string& err, const mstar_prefix_group* groups,
+                    int32_t num_groups, const int32_t* members, int32_t num_members) {
     if (!params) { err = "params is NULL"; return MSTAR_ERR_INVALID_ARG; }
     if (num_seqs < 0 || num_segs < 0) { err = "negative count"; return MSTAR_ERR_INVALID_ARG; }
     if (num_seqs > 0 && (!seqs || !masks)) { err = "seqs/masks is NULL"; return MSTAR_ERR_INVALID_ARG; }
@@ -162,7 +164,10 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         err = "FORCE_SPLIT and NO_SPLIT are exclusive";
         return MSTAR_ERR_INVALID_ARG;
     }
-    if (P.flags & ~(MSTAR_FLAG_FORCE_SPLIT | MSTAR_FLAG_NO_SPLIT)) { err = "unknown flag"; return MSTAR_ERR_INVALID_ARG; }
+    if (P.flags & ~(MSTAR_FLAG_FORCE_SPLIT | MSTAR_FLAG_NO_SPLIT | MSTAR_FLAG_CASCADE_ALL)) {
+        err = "unknown flag";
+        return MSTAR_ERR_INVALID_ARG;
+    }
 
     plan = HostPlan();
     plan.params = P;
@@ -217,6 +222,57 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     }
     plan.total_q = (int32_t)total_q;
 
+    // ---- shared-prefix groups (cascade) ------------------------------------
+    // group_of[r]: the group of request r or -1; member_rows[r]: query rows of
+    // the group's members before r (its rows start there in the group's list)
+    std::vector<int32_t> group_of(num_seqs, -1);
+    std::vector<int64_t> member_rows(num_seqs, 0);
+    std::vector<int64_t> group_rows(std::max(num_groups, 0), 0);
+    std::vector<std::vector<int32_t>> joined(std::max(num_groups, 0));  // members in the cascade
+    std::vector<char> listed(num_seqs, 0);
+    if (num_groups < 0 || num_members < 0) { err = "negative group count"; return MSTAR_ERR_INVALID_ARG; }
+    if ((num_groups > 0 && !groups) || (num_members > 0 && !members)) {
+        err = "groups/members is NULL";
+        return MSTAR_ERR_INVALID_ARG;
+    }
+    if (num_groups > 0 && P.dtype == MSTAR_DTYPE_F32) { err = "prefix groups need the bf16 dtype"; return MSTAR_ERR_UNSUPPORTED; }
+    for (int32_t g = 0; g < num_groups; ++g) {
+        const mstar_prefix_group& gr = groups[g];
+        char buf[160];
+        if (gr.member_count < 1 || gr.member_begin < 0 || (int64_t)gr.member_begin + gr.member_count > num_members ||
+            gr.prefix_len <= 0 || gr.prefix_len % kPage != 0) {
+            snprintf(buf, sizeof buf, "prefix group %d: bad member range or prefix_len (a positive multiple of 16)", g);
+            err = buf;
+            return MSTAR_ERR_INVALID_ARG;
+        }
+        for (int32_t k = 0; k < gr.member_count; ++k) {
+            const int32_t r = members[gr.member_begin + k];
+            if (r < 0 || r >= num_seqs || listed[r]) {
+                snprintf(buf, sizeof buf, "prefix group %d: member %d out of range or in two groups", g, r);
+                err = buf;
+                return MSTAR_ERR_INVALID_ARG;
+            }
+            listed[r] = 1;
+            const mstar_seq_desc& s = seqs[r];
+            // intervals never shrink from one row to the next: the first row
+            // decides hi >= prefix_len, the last one lo == 0
+            if (s.kv_len < gr.prefix_len ||
+                (s.q_len > 0 && (iv[r].hi[0] < gr.prefix_len || iv[r].lo[s.q_len - 1] != 0))) {
+                snprintf(buf, sizeof buf, "prefix group %d: a query row of request %d does not see the whole prefix",
+                         g, r);
+                err = buf;
+                return MSTAR_ERR_INVALID_ARG;
+            }
+            // a member whose rows fill tiles already reads each prefix tile
+            // once per 128 rows: the cascade would only add the merge
+            if (!(P.flags & MSTAR_FLAG_CASCADE_ALL) && (int64_t)s.q_len * G > kDecodeMaxRows) continue;
+            group_of[r] = g;
+            member_rows[r] = group_rows[g];
+            group_rows[g] += s.q_len;
+            joined[g].push_back(r);
+        }
+    }
+
     plan.seqs.resize(num_seqs);
     plan.key_lo.assign(num_seqs, 0);
     plan.key_hi.assign(num_seqs, 0);
@@ -257,10 +313,15 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             continue;
         }
         const int64_t R = (int64_t)s.q_len * G;
+        // a cascade member's own work covers the keys after the shared prefix
+        const bool member = group_of[r] >= 0;
+        const int32_t own0 = member ? groups[group_of[r]].prefix_len : 0;
+        if (member && v.hi[s.q_len - 1] <= own0) continue;  // the prefix is all it sees
         if (R <= kDecodeMaxRows) {
             for (int32_t kvh = 0; kvh < P.num_kv_heads; ++kvh) {
-                Unit u{r, kvh, 0, (int32_t)R, align_down16(v.lo[0]), v.hi[s.q_len - 1], 0};
+                Unit u{r, kvh, 0, (int32_t)R, member ? own0 : align_down16(v.lo[0]), v.hi[s.q_len - 1], 0};
                 u.cost = (int64_t)(u.k_end - u.k_begin);
+                u.partial = member;
                 few_units.push_back(u);
             }
             plan.decode_rb = std::max<int32_t>(plan.decode_rb, R <= 16 ? 1 : R <= 32 ? 2 : 4);
@@ -268,7 +329,11 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             // one unit per row tile, shared by every query head
             for (int32_t row0 = 0; row0 < s.q_len; row0 += kTileRows) {
                 const int32_t nr = std::min(kTileRows, s.q_len - row0);
-                Unit u{r, -1, row0, nr, align_down16(v.lo[row0]), v.hi[row0 + nr - 1], 0};
+                const int32_t kb = member ? own0 : align_down16(v.lo[row0]);
+                const int32_t ke = v.hi[row0 + nr - 1];
+                if (ke <= kb) continue;  // rows that see only the prefix
+                Unit u{r, -1, row0, nr, kb, ke, 0};
+                u.partial = member;
                 tile_units.push_back(u);
             }
         }
@@ -286,6 +351,84 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
 
     // ---- 4. key splitting ---------------------------------------------------
     int64_t slot = 0;
+    // Cascade: per (group, KV head) a row list of (member, query row, query
+    // head) in member order, cut into 128-row items over the prefix keys, the
+    // prefix cut into equal chunks when the items alone cannot fill the GPU.
+    // The partial of chunk c, list row j sits at slot base + c * R + j.
+    struct CascSlots { int64_t base = 0, rows = 0, chunks = 1; };
+    std::vector<CascSlots> casc((size_t)std::max(num_groups, 0) * P.num_kv_heads);
+    if (num_groups > 0) {
+        int64_t tiles = 0;
+        for (int32_t g = 0; g < num_groups; ++g) tiles += ceil_div(group_rows[g] * G, kTileRows) * P.num_kv_heads;
+        for (int32_t g = 0; g < num_groups; ++g) {
+            const mstar_prefix_group& gr = groups[g];
+            const int64_t R = group_rows[g] * G;
+            if (R == 0) continue;  // no member joined, or none has a query row
+            int64_t nch = 1;
+            if (!(P.flags & MSTAR_FLAG_NO_SPLIT) && tiles > 0 && tiles < 512) nch = ceil_div(512, tiles);
+            if (P.flags & MSTAR_FLAG_FORCE_SPLIT) nch = 3;
+            nch = std::max<int64_t>(1, std::min<int64_t>(nch, gr.prefix_len / (2 * kTileKeys)));
+            const int64_t cs = ceil_div(ceil_div(gr.prefix_len, nch), kTileKeys) * kTileKeys;
+            nch = ceil_div(gr.prefix_len, cs);
+            for (int32_t kvh = 0; kvh < P.num_kv_heads; ++kvh) {
+                CascSlots& cslot = casc[(size_t)g * P.num_kv_heads + kvh];
+                cslot.base = slot;
+                cslot.rows = R;
+                cslot.chunks = nch;
+                const int64_t row_off = (int64_t)plan.casc_rows.size() / 2;
+                for (const int32_t r : joined[g]) {
+                    for (int32_t i = 0; i < seqs[r].q_len; ++i)
+                        for (int32_t h = kvh * G; h < (kvh + 1) * G; ++h) {
+                            plan.casc_rows.push_back(seqs[r].q_start + i);
+                            plan.casc_rows.push_back(h);
+                        }
+                }
+                for (int64_t c = 0; c < nch; ++c)
+                    for (int64_t b0 = 0; b0 < R; b0 += kTileRows) {
+                        WorkItem w;
+                        w.seq = joined[g][0];
+                        w.head = kvh;
+                        w.row0 = (int32_t)(row_off + b0);
+                        w.nrows = (int32_t)std::min<int64_t>(kTileRows, R - b0);
+                        w.k_begin = (int32_t)(c * cs);
+                        w.k_end = (int32_t)std::min<int64_t>((c + 1) * cs, gr.prefix_len);
+                        w.part = (int32_t)(slot + c * R + b0);
+                        w.head_stride = -1;
+                        plan.cascade.push_back(w);
+                    }
+                slot += nch * R;
+            }
+        }
+        if (plan.casc_rows.size() / 2 > (size_t)INT32_MAX) { err = "too many cascade rows"; return MSTAR_ERR_INVALID_ARG; }
+    }
+    // prefix slot set of (request r, its query row i, query head h)
+    auto prefix_slots = [&](MergeItem& m, int32_t r, int32_t i, int32_t h) {
+        if (group_of[r] < 0) {
+            m.pad0 = m.pad1 = m.pad2 = 0;
+            return;
+        }
+        const int32_t kvh = h / G;
+        const CascSlots& cslot = casc[(size_t)group_of[r] * P.num_kv_heads + kvh];
+        m.pad0 = (int32_t)(cslot.base + (member_rows[r] + i) * G + (h - kvh * G));
+        m.pad1 = (int32_t)cslot.rows;
+        m.pad2 = (int32_t)cslot.chunks;
+    };
+    // members that see nothing past the prefix: the merge reads the prefix partials alone
+    for (int32_t r = 0; r < num_seqs; ++r) {
+        if (group_of[r] < 0 || seqs[r].q_len == 0) continue;
+        if (iv[r].hi[seqs[r].q_len - 1] > groups[group_of[r]].prefix_len) continue;
+        for (int32_t i = 0; i < seqs[r].q_len; ++i)
+            for (int32_t h = 0; h < P.num_qo_heads; ++h) {
+                MergeItem m;
+                m.row = seqs[r].q_start + i;
+                m.head = h;
+                m.slot0 = 0;
+                m.stride = 0;
+                m.nslots = 0;
+                prefix_slots(m, r, i, h);
+                plan.merges.push_back(m);
+            }
+    }
     // Few-row units are cut into pieces of exactly `chunk` keys plus one shorter
     // remainder: with longest-first order the equal pieces fill every CU evenly
     // and the remainders fill the gaps (a simulation of the decode batch on 256
@@ -315,11 +458,12 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             w.nrows = u.nrows;
             w.k_begin = (int32_t)(u.k_begin + c * cs);
             w.k_end = (int32_t)std::min<int64_t>(u.k_begin + (c + 1) * cs, u.k_end);
-            w.part = nch > 1 ? (int32_t)(slot + c * u.nrows) : -1;
-            w.head_stride = (nch > 1 && !few) ? (int32_t)(nch * u.nrows) : -1;
+            const bool partial = nch > 1 || u.partial;
+            w.part = partial ? (int32_t)(slot + c * u.nrows) : -1;
+            w.head_stride = (partial && !few) ? (int32_t)(nch * u.nrows) : -1;
             dst.push_back(w);
         }
-        if (nch > 1) {
+        if (nch > 1 || u.partial) {
             const SeqInfo& si = plan.seqs[u.seq];
             for (int64_t h = 0; h < heads; ++h) {
                 for (int32_t r = 0; r < u.nrows; ++r) {
@@ -330,7 +474,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                     m.slot0 = (int32_t)(slot + h * nch * u.nrows + r);
                     m.stride = u.nrows;
                     m.nslots = (int32_t)nch;
-                    m.pad0 = m.pad1 = m.pad2 = 0;
+                    prefix_slots(m, u.seq, few ? rr / G : rr, m.head);
                     plan.merges.push_back(m);
                 }
             }
@@ -386,55 +530,89 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     lpt(plan.f32, true);
 
     // ---- 6. launch order of the multi-row workgroups ----------------------------
-    // One workgroup per (tile item, query head).  The hardware deals workgroup
-    // b to XCD b % 8, and each XCD has its own L2.  Every workgroup that reads
-    // the same K/V pages -- the items of one request and the G query heads of
-    // one KV head -- goes to the same XCD, consecutively, so they run together
-    // and read each K/V tile from that L2.  Groups go to the least-loaded XCD,
-    // largest first; inside a group the items keep their longest-first order.
-    {
-        struct Group { int64_t cost = 0; int32_t seq = 0, kvh = 0; std::vector<int32_t> items; };
-        std::vector<Group> groups;
+    // One workgroup per (tile item, query head); one per cascade item (its rows
+    // name their heads; the order entry carries a head of its KV head).  The
+    // hardware deals workgroup b to XCD b % 8, and each XCD has its own L2.
+    // Every workgroup that reads the same K/V pages -- the items of one
+    // request and the G query heads of one KV head -- goes to the same XCD,
+    // consecutively, so they run together and read each K/V tile from that
+    // L2.  A group costlier than an even share of one XCD is cut into
+    // consecutive runs of items (one such group alone would otherwise leave
+    // the other XCDs idle).  Groups go to the least-loaded XCD, largest first;
+    // inside a group the items keep their order.
+    auto launch_order = [&](const std::vector<WorkItem>& items, bool per_head, std::vector<int32_t>& order) {
+        struct Group { int64_t cost = 0; int32_t kvh = 0; std::vector<int32_t> items; std::vector<int64_t> costs; };
+        std::vector<Group> whole, groups_;
         std::vector<int64_t> index((size_t)num_seqs * P.num_kv_heads, -1);
-        for (size_t i = 0; i < plan.tiles.size(); ++i) {
-            const WorkItem& w = plan.tiles[i];
-            const int64_t pairs = visible_in(w) * G;
+        int64_t total = 0;
+        for (size_t i = 0; i < items.size(); ++i) {
+            const WorkItem& w = items[i];
+            const int64_t pairs = per_head ? visible_in(w) * G : (int64_t)w.nrows * (w.k_end - w.k_begin);
             for (int32_t kvh = 0; kvh < P.num_kv_heads; ++kvh) {
+                if (!per_head && kvh != w.head) continue;
                 int64_t& gi = index[(size_t)w.seq * P.num_kv_heads + kvh];
                 if (gi < 0) {
-                    gi = (int64_t)groups.size();
-                    groups.emplace_back();
-                    groups.back().seq = w.seq;
-                    groups.back().kvh = kvh;
+                    gi = (int64_t)whole.size();
+                    whole.emplace_back();
+                    whole.back().kvh = kvh;
                 }
-                groups[gi].items.push_back((int32_t)i);
-                groups[gi].cost += pairs + 1;  // +1: an empty item still costs a workgroup
+                whole[gi].items.push_back((int32_t)i);
+                whole[gi].costs.push_back(pairs + 1);  // +1: an empty item still costs a workgroup
+                whole[gi].cost += pairs + 1;
+                total += pairs + 1;
             }
         }
-        std::stable_sort(groups.begin(), groups.end(), [](const Group& x, const Group& y) { return x.cost > y.cost; });
         constexpr int kXcds = 8;
+        const int64_t share = ceil_div(total, kXcds);
+        for (Group& g : whole) {
+            if (g.cost <= share) {
+                groups_.push_back(std::move(g));
+                continue;
+            }
+            Group piece;
+            piece.kvh = g.kvh;
+            for (size_t k = 0; k < g.items.size(); ++k) {
+                if (!piece.items.empty() && piece.cost + g.costs[k] > share) {
+                    groups_.push_back(std::move(piece));
+                    piece = Group();
+                    piece.kvh = g.kvh;
+                }
+                piece.items.push_back(g.items[k]);
+                piece.cost += g.costs[k];
+            }
+            groups_.push_back(std::move(piece));
+        }
+        std::stable_sort(groups_.begin(), groups_.end(), [](const Group& x, const Group& y) { return x.cost > y.cost; });
         std::vector<int32_t> lists[kXcds];
         int64_t load[kXcds] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (const Group& g : groups) {
+        for (const Group& g : groups_) {
             int x = 0;
             for (int k = 1; k < kXcds; ++k)
                 if (load[k] < load[x]) x = k;
             load[x] += g.cost;
-            for (int32_t item : g.items)
-                for (int32_t h = g.kvh * G; h < (g.kvh + 1) * G; ++h) {
+            for (int32_t item : g.items) {
+                const int32_t h0 = per_head ? g.kvh * G : g.kvh * G;
+                const int32_t h1 = per_head ? (g.kvh + 1) * G : g.kvh * G + 1;
+                for (int32_t h = h0; h < h1; ++h) {
                     lists[x].push_back(item);
                     lists[x].push_back(h);
                 }
+            }
         }
         size_t slots = 0;
         for (int x = 0; x < kXcds; ++x) slots = std::max(slots, lists[x].size() / 2);
-        if (slots * kXcds > (size_t)INT32_MAX / 2) { err = "too many tile workgroups"; return MSTAR_ERR_INVALID_ARG; }
-        plan.tile_order.assign(2 * slots * kXcds, -1);  // padding workgroups exit at once
+        if (slots * kXcds > (size_t)INT32_MAX / 2) return false;
+        order.assign(2 * slots * kXcds, -1);  // padding workgroups exit at once
         for (int x = 0; x < kXcds; ++x)
             for (size_t k = 0; 2 * k < lists[x].size(); ++k) {
-                plan.tile_order[2 * (k * kXcds + x)] = lists[x][2 * k];
-                plan.tile_order[2 * (k * kXcds + x) + 1] = lists[x][2 * k + 1];
+                order[2 * (k * kXcds + x)] = lists[x][2 * k];
+                order[2 * (k * kXcds + x) + 1] = lists[x][2 * k + 1];
             }
+        return true;
+    };
+    if (!launch_order(plan.tiles, true, plan.tile_order) || !launch_order(plan.cascade, false, plan.casc_order)) {
+        err = "too many tile workgroups";
+        return MSTAR_ERR_INVALID_ARG;
     }
     return MSTAR_OK;
 }

@@ -26,6 +26,12 @@ struct HostPlan {
     std::vector<WorkItem> f32;            // fp32 kernel
     std::vector<MergeItem> merges;        // (row, head) outputs assembled from partials
     std::vector<WorkItem> appends;        // KV append: up to kAppendRows new rows of one request each
+    // shared-prefix cascade: items over a group's prefix keys (seq = the first
+    // member, head = KV head, rows row0 .. row0 + nrows - 1 of casc_rows), the
+    // (packed query row, query head) of every row, and their launch order
+    std::vector<WorkItem> cascade;
+    std::vector<int32_t> casc_rows;
+    std::vector<int32_t> casc_order;
     int64_t visible_pairs = 0;
     int64_t partial_slots = 0;
 };
@@ -34,6 +40,8 @@ struct HostPlan {
 // with a message in `err`.
 int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                     const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segs,
-                    int32_t num_segs, HostPlan& plan, std::string& err);
+                    int32_t num_segs, HostPlan& plan, std::string& err,
+                    const mstar_prefix_group* groups = nullptr, int32_t num_groups = 0,
+                    const int32_t* members = nullptr, int32_t num_members = 0);
 
 }  // namespace mstar

@@ -199,13 +199,22 @@ def test_tile_launch_order_groups_kv_readers_on_one_xcd(name):
     real = [(i, h) for i, h in order.tolist() if i >= 0]
     assert all(i == -1 and h == -1 for i, h in order.tolist() if i < 0)
     assert sorted(real) == sorted((i, h) for i in range(len(items)) for h in range(b.num_qo_heads))
-    xcd_of, pos = {}, {}
+    _check_xcd_runs(order, items, G, balanced=name != "mixed")
+    pl.destroy()
+
+
+def _check_xcd_runs(order, items, G, balanced):
+    """Each (request, KV head) group's workgroups are consecutive on an XCD;
+    a group on several XCDs holds a run of consecutive items on each."""
+    runs = {}  # group -> {xcd: [items]}
     lists = {x: [] for x in range(8)}
     for wg, (i, h) in enumerate(order.tolist()):
         if i < 0:
             continue
         grp = (int(items[i][0]), h // G)
-        assert xcd_of.setdefault(grp, wg % 8) == wg % 8
+        lst = runs.setdefault(grp, {}).setdefault(wg % 8, [])
+        if not lst or lst[-1] != i:
+            lst.append(i)
         lists[wg % 8].append(grp)
     for x, seq in lists.items():  # a group's workgroups are consecutive on its XCD
         seen = []
@@ -213,11 +222,153 @@ def test_tile_launch_order_groups_kv_readers_on_one_xcd(name):
             if not seen or seen[-1] != grp:
                 assert grp not in seen, (x, grp)
                 seen.append(grp)
+    for grp, per_xcd in runs.items():
+        pieces = sorted(per_xcd.values())
+        flat = [i for p in pieces for i in p]
+        assert flat == sorted(flat) and len(set(flat)) == len(flat)  # consecutive runs of the group's items
     sizes = {}
     for seq in lists.values():
         for grp in seq:
             sizes[grp] = sizes.get(grp, 0) + 1
     counts = [len(seq) for seq in lists.values()]
-    if name != "mixed":  # equal groups: workgroup counts per XCD within one group
+    if balanced:  # equal groups: workgroup counts per XCD within one group
         assert max(counts) - min(counts) <= max(sizes.values())
+    return counts
+
+
+def test_cascade_launch_order_spreads_one_group_over_every_xcd():
+    """The shared-prefix decode has one cascade group per KV head (4 groups of
+    equal cost): each is cut into runs so that all 8 XCDs get work."""
+    b = W.FULL_SIZE["shared_prefix_decode_bf16"]()
+    pl = plan_for(b, attn.FLAG_HOST_ONLY, cascade=True)
+    items = pl.items(4)
+    order = pl.tile_order(cascade=True)
+    G = b.num_qo_heads // b.num_kv_heads
+    real = sorted(i for i, _ in order.tolist() if i >= 0)
+    assert real == list(range(len(items)))
+    for i, h in order.tolist():
+        if i >= 0:
+            assert h // G == items[i][1]
+    counts = _check_xcd_runs(order, items, G, balanced=True)
+    assert min(counts) > 0 and max(counts) - min(counts) <= 1, counts
     pl.destroy()
+
+
+CASCADE = ["rollout_bf16", "cfg_labels_bf16", "mixed", "shared_prefix_decode_bf16"]
+
+
+@pytest.mark.parametrize("name", CASCADE)
+@pytest.mark.parametrize("flags", [0, attn.FLAG_FORCE_SPLIT, attn.FLAG_NO_SPLIT])
+def test_cascade_plan_covers_each_visible_pair_once_and_merges_read_written_slots(name, flags):
+    """A cascade plan: cascade items cover the group's prefix keys for every
+    member row and head, the members' own items the rest; every visible
+    (row, key, head) exactly once; each merge record reads exactly the partial
+    slots written for its (row, head)."""
+    b = W.reduced(name)
+    pl = plan_for(b, flags | attn.FLAG_HOST_ONLY | attn.FLAG_CASCADE_ALL, cascade=True)
+    G = b.num_qo_heads // b.num_kv_heads
+    req_of_row = {}
+    for r in range(b.num_seqs):
+        q_len, _, qs = (int(x) for x in b.seqs[r])
+        for i in range(q_len):
+            req_of_row[qs + i] = (r, i)
+    cover, written = {}, {}
+
+    def add(key, kb, ke, slot):
+        cover.setdefault(key, []).append((kb, ke))
+        if slot >= 0:
+            assert slot not in written
+            written[slot] = key
+
+    for kind in (0, 1):
+        for seq, head, row0, nrows, kb, ke, part, hs in pl.items(kind):
+            for h in (range(b.num_qo_heads) if kind == 0 else [head]):
+                for r in range(nrows):
+                    rr = row0 + r
+                    key = (seq, rr // G, h * G + rr % G) if kind == 1 else (seq, rr, h)
+                    slot = -1 if part < 0 else part + r + (h * hs if kind == 0 else 0)
+                    add(key, kb, ke, slot)
+    rows = pl.items(5)
+    members = {r for mem, _ in b.prefix_groups for r in mem}
+    for seq, kvh, row0, nrows, kb, ke, part, _ in pl.items(4):
+        assert seq in members and part >= 0
+        for r in range(nrows):
+            qrow, h = int(rows[row0 + r][0]), int(rows[row0 + r][1])
+            assert h // G == kvh
+            req, i = req_of_row[qrow]
+            assert req in members
+            add((req, i, h), kb, ke, part + r)
+    for r in range(b.num_seqs):
+        q_len, L, _ = (int(x) for x in b.seqs[r])
+        vis = visible_matrix(q_len, L, block_ids(b.seq_segments(r), L), int(b.masks[r, 2]))
+        for i in range(q_len):
+            for h in range(b.num_qo_heads):
+                ranges = sorted(cover[(r, i, h)])
+                for (a0, a1), (c0, c1) in zip(ranges[:-1], ranges[1:]):
+                    assert a1 <= c0
+                covered = np.zeros(L, dtype=bool)
+                for a0, a1 in ranges:
+                    covered[a0:a1] = True
+                assert covered[np.nonzero(vis[i])[0]].all()
+    slots_cap = pl.stats()["partial_slots"]
+    assert written and max(written) < slots_cap and min(written) >= 0
+    merged = set()
+    n_written = {}
+    for k in written.values():
+        n_written[k] = n_written.get(k, 0) + 1
+    for row, head, s0, st, ns, p0, pst, pns in pl.items(3):
+        slots = [s0 + k * st for k in range(ns)] + [p0 + k * pst for k in range(pns)]
+        req, i = req_of_row[int(row)]
+        assert {written[s] for s in slots} == {(req, i, int(head))}
+        assert len(slots) == n_written[(req, i, int(head))]
+        merged.add((req, i, int(head)))
+    for (req, i, h) in cover:  # every member output is merged
+        if req in members:
+            assert (req, i, h) in merged
+    pl.destroy()
+
+
+@pytest.mark.parametrize("name", CASCADE)
+def test_cascade_takes_only_decode_like_members_by_default(name):
+    """Without FLAG_CASCADE_ALL only members with query rows x group size
+    <= 64 join; a plan whose members all fill tiles equals the plain plan."""
+    b = W.reduced(name)
+    G = b.num_qo_heads // b.num_kv_heads
+    pl = plan_for(b, attn.FLAG_HOST_ONLY, cascade=True)
+    plain = plan_for(b, attn.FLAG_HOST_ONLY)
+    rows = pl.items(5)
+    joined = {int(r) for mem, _ in b.prefix_groups for r in mem if int(b.seqs[r, 0]) * G <= 64}
+    qrow_req = {int(b.seqs[r, 2]) + i: r for r in range(b.num_seqs) for i in range(int(b.seqs[r, 0]))}
+    assert {qrow_req[int(x[0])] for x in rows} == {r for r in joined if b.seqs[r, 0] > 0}
+    if not joined:
+        for kind in (0, 1, 3):
+            assert np.array_equal(pl.items(kind), plain.items(kind))
+        assert len(pl.items(4)) == 0
+    pl.destroy()
+    plain.destroy()
+
+
+def test_cascade_rejects_bad_groups():
+    b = W.reduced("rollout_bf16")
+    args = (b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, b.seqs, b.masks, b.segments,
+            b.block_table.shape[1], b.num_pages, b.sm_scale, attn.FLAG_HOST_ONLY)
+    for groups in ([([0, 1], 30)],            # prefix not a multiple of 16
+                   [([0, 0], 64)],            # repeated member
+                   [([0, 99], 64)],           # member out of range
+                   [([0, 1], 0)],             # empty prefix
+                   [([0, 1], 512)]):          # longer than the members' kv_len
+        with pytest.raises(attn.MStarError):
+            attn.plan(*args, prefix_groups=groups).destroy()
+    # a member query row that does not see the whole prefix: causal decode rows inside the prefix
+    c = W.reduced("text_latent_bf16")  # text rows are causal: row 0 sees one key
+    with pytest.raises(attn.MStarError) as ei:
+        attn.plan(c.num_qo_heads, c.num_kv_heads, c.head_dim, c.dtype, c.seqs, c.masks, c.segments,
+                  c.block_table.shape[1], c.num_pages, c.sm_scale, attn.FLAG_HOST_ONLY,
+                  prefix_groups=[([0, 1], 32)]).destroy()
+    assert "whole prefix" in str(ei.value)
+    f = W.reduced("tiny_causal_f32")
+    with pytest.raises(attn.MStarError) as ei:
+        attn.plan(f.num_qo_heads, f.num_kv_heads, f.head_dim, f.dtype, f.seqs, f.masks, f.segments,
+                  f.block_table.shape[1], f.num_pages, f.sm_scale, attn.FLAG_HOST_ONLY,
+                  prefix_groups=[([0, 1], 16)]).destroy()
+    assert ei.value.code == attn.ERR_UNSUPPORTED

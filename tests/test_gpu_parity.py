@@ -38,7 +38,8 @@ def _oracle(b, t):
 
 
 REDUCED = ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16", "rollout_bf16",
-           "cfg_labels_bf16", "mixed"]
+           "cfg_labels_bf16", "shared_prefix_decode_bf16", "mixed"]
+CASCADE = ["rollout_bf16", "cfg_labels_bf16", "shared_prefix_decode_bf16", "mixed"]
 FLAGS = {"auto": 0, "force_split": attn.FLAG_FORCE_SPLIT, "no_split": attn.FLAG_NO_SPLIT}
 
 
@@ -50,6 +51,20 @@ def test_reduced_parity(name, flag):
     out, lse = run_gpu(b, t, FLAGS[flag])
     ro, rl = _oracle(b, t)
     _compare(b, out, lse, ro, rl, f"{name}/{flag}")
+
+
+@pytest.mark.parametrize("flag", list(FLAGS))
+@pytest.mark.parametrize("name", CASCADE)
+def test_cascade_parity(name, flag):
+    """Shared-prefix cascade plans (prefix attended once for all members'
+    rows, own keys separately, merged by log-sum-exp) against the oracle,
+    every member in the cascade and (default) only the decode-like ones."""
+    b = W.reduced(name)
+    t = W.make_tensors_torch(b, DEV, poison_unused=True)
+    ro, rl = _oracle(b, t)
+    for extra, tag in ((attn.FLAG_CASCADE_ALL, "all"), (0, "default")):
+        out, lse = run_gpu(b, t, FLAGS[flag] | extra, cascade=True)
+        _compare(b, out, lse, ro, rl, f"{name}/cascade-{tag}/{flag}")
 
 
 @pytest.mark.parametrize("seed", [1, 2])
@@ -138,15 +153,18 @@ def test_fwd_rejects_wrong_shapes_and_small_workspace():
 # Full sizes: sampled outputs against the oracle, and a property of every row.
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("name", ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16",
-                                  "rollout_bf16", "cfg_labels_bf16"])
-def test_full_size_sampled(name):
+@pytest.mark.parametrize("name,cascade", [("tiny_causal_f32", False), ("decode_bf16", False),
+                                          ("text_latent_bf16", False), ("stream_window_bf16", False),
+                                          ("rollout_bf16", False), ("cfg_labels_bf16", False),
+                                          ("shared_prefix_decode_bf16", False), ("shared_prefix_decode_bf16", True),
+                                          ("rollout_bf16", True), ("cfg_labels_bf16", True)])
+def test_full_size_sampled(name, cascade):
     import torch
 
     b = W.FULL_SIZE[name]()
     print(f"{name}: generating", flush=True)
     t = W.make_tensors_torch(b, DEV)
-    out, lse = run_gpu(b, t)
+    out, lse = run_gpu(b, t, attn.FLAG_CASCADE_ALL if cascade else 0, cascade=cascade)
     torch.cuda.synchronize()
     print(f"{name}: fwd done", flush=True)
     # every output is a convex combination of value rows
@@ -168,5 +186,6 @@ def test_full_size_sampled(name):
     got_l = np.array([float(lse[rows[sb.seqs[j, 2] + i], h]) for j, i, h in picks])
     tol_o, tol_l = TOL[b.dtype]
     eo, el = float(np.abs(got_o - ro).max()), float(np.abs(got_l - rl).max())
-    print(f"{name} full size, {len(picks)} sampled rows: max|dout|={eo:.3e} max|dlse|={el:.3e}", flush=True)
+    print(f"{name} full size{' (cascade)' if cascade else ''}, {len(picks)} sampled rows: "
+          f"max|dout|={eo:.3e} max|dlse|={el:.3e}", flush=True)
     assert eo <= tol_o and el <= tol_l

@@ -28,6 +28,9 @@ per-layer attention shapes and its datasets are not used):
                           one paged pool, the image-dropped label reading the
                           conditional label's text pages in place (Sec. 4.1;
                           App. F, CFG Walk).
+* ``shared_prefix_decode_bf16`` - one new token for each of many requests over
+                          one shared context plus their own tokens (candidates
+                          continued from one context, App. A).
 * ``mixed``             - requests of all the kinds above in one launch (one
                           ``LLM`` replica serving every Walk, Sec. 3.2).
 
@@ -77,6 +80,10 @@ class Batch:
     page_size: int = PAGE
     sm_scale: float = 0.0
     seed: int = 0
+    # shared-prefix groups: [(member request indices, prefix_len), ...]; the
+    # members' block tables agree on the first prefix_len / 16 pages and all
+    # their query rows see those keys (for a cascade plan)
+    prefix_groups: Optional[list] = None
 
     def __post_init__(self):
         if self.sm_scale == 0.0:
@@ -203,7 +210,27 @@ def rollout_bf16(seed: int = 0, n: int = 300, prefix: int = 2048, frames: int = 
     kv = [L] * n
     bt, pool = _layout_pages(kv, None, _rng(seed, _SUB_PERM), shared_prefix_pages=prefix // PAGE)
     segs = [[(0, prefix, SEG_FULL, 0), (prefix, q, SEG_BLOCKS, frame)] for _ in range(n)]
-    return _finish("rollout_bf16", hq, hkv, d, "bf16", [q] * n, kv, segs, [0] * n, bt, pool, seed)
+    b = _finish("rollout_bf16", hq, hkv, d, "bf16", [q] * n, kv, segs, [0] * n, bt, pool, seed)
+    b.prefix_groups = [(list(range(n)), prefix)]
+    return b
+
+
+def shared_prefix_decode_bf16(seed: int = 0, n: int = 128, prefix: int = 4096, own_min: int = 256,
+                              own_max: int = 1024, hq: int = 28, hkv: int = 4, d: int = 128) -> Batch:
+    """n requests decoding one token each over one shared ``prefix``-token
+    context (its pages are referenced by every block table) followed by their
+    own ``own ~ U{own_min..own_max}`` tokens: K candidates or samples continued
+    from one context in one batched step (App. A, V-JEPA 2 MPC Walk; Sec. 4.1,
+    contexts as labels over one pool).  One prefix group holds every request."""
+    if prefix % PAGE:
+        raise ValueError("shared prefix must be page aligned")
+    own = _rng(seed, _SUB_LENGTHS).integers(own_min, own_max + 1, size=n)
+    kv = [prefix + int(x) for x in own]
+    bt, pool = _layout_pages(kv, None, _rng(seed, _SUB_PERM), shared_prefix_pages=prefix // PAGE)
+    segs = [[(0, L, SEG_CAUSAL, 0)] for L in kv]
+    b = _finish("shared_prefix_decode_bf16", hq, hkv, d, "bf16", [1] * n, kv, segs, [0] * n, bt, pool, seed)
+    b.prefix_groups = [(list(range(n)), prefix)]
+    return b
 
 
 def cfg_labels_bf16(seed: int = 0, n: int = 2, text: int = 256, image: int = 4096, latent: int = 4096,
@@ -245,8 +272,10 @@ def cfg_labels_bf16(seed: int = 0, n: int = 2, text: int = 256, image: int = 409
         else:
             bt[r, :own[r]] = perm[cur:cur + own[r]]
         cur += own[r]
-    return _finish("cfg_labels_bf16", hq, hkv, d, "bf16", q_lens, kv_lens, seg_lists, [0] * len(q_lens),
-                   bt, pool, seed)
+    b = _finish("cfg_labels_bf16", hq, hkv, d, "bf16", q_lens, kv_lens, seg_lists, [0] * len(q_lens),
+                bt, pool, seed)
+    b.prefix_groups = [([3 * i, 3 * i + 2], text) for i in range(n)]  # conditional + image dropped
+    return b
 
 
 def mixed(seed: int = 0, hq: int = 8, hkv: int = 2, d: int = 128, dtype: str = "bf16",
@@ -297,7 +326,9 @@ def mixed(seed: int = 0, hq: int = 8, hkv: int = 2, d: int = 128, dtype: str = "
             off = shared_pages
         bt[r, off:off + own[r]] = perm[cur:cur + own[r]]
         cur += own[r]
-    return _finish("mixed", hq, hkv, d, dtype, q_lens, kv_lens, seg_lists, windows, bt, pool, seed)
+    b = _finish("mixed", hq, hkv, d, dtype, q_lens, kv_lens, seg_lists, windows, bt, pool, seed)
+    b.prefix_groups = [(list(range(kv_rollout_start, kv_rollout_start + n_roll)), prefix)]
+    return b
 
 
 FULL_SIZE = {
@@ -307,6 +338,7 @@ FULL_SIZE = {
     "stream_window_bf16": stream_window_bf16,
     "rollout_bf16": rollout_bf16,
     "cfg_labels_bf16": cfg_labels_bf16,
+    "shared_prefix_decode_bf16": shared_prefix_decode_bf16,
 }
 
 
@@ -326,6 +358,8 @@ def reduced(name: str, seed: int = 0) -> Batch:
         return rollout_bf16(seed, n=5, prefix=64, frames=4, frame=40)
     if name == "cfg_labels_bf16":
         return cfg_labels_bf16(seed, n=2, text=32, image=101, latent=70, hq=7, hkv=1)
+    if name == "shared_prefix_decode_bf16":
+        return shared_prefix_decode_bf16(seed, n=37, prefix=320, own_min=1, own_max=150, hq=8, hkv=2)
     if name == "mixed":
         return mixed(seed)
     raise KeyError(name)
