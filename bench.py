@@ -381,7 +381,7 @@ def main():
     traffic_note = "no counter run recorded for this kernel source"
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
-            rec = json.load(f).get(args.workload)
+            rec = json.load(f).get(args.workload + ("+cascade" if args.cascade else ""))
         if rec and rec.get("kernel_src_sha") == kernel_source_sha():
             traffic = rec["hbm_bytes_per_launch"]
             traffic_note = rec.get("note", "")

@@ -137,16 +137,20 @@ __device__ __forceinline__ void row_interval(const KArgs& a, const SeqInfo& si, 
 constexpr float kLazy = 8.0f;
 
 // Balanced reductions over the 4*NB score values a lane holds for one row.
+// Three-input maximum (one v_max3_f32).
+__device__ __forceinline__ float max3(float a, float b, float c) { return fmax_num(fmax_num(a, b), c); }
 template <int NB>
 __device__ __forceinline__ float tree_max(const f32x4 (&s)[NB]) {
-    float v[NB];
-#pragma unroll
-    for (int kb = 0; kb < NB; ++kb) v[kb] = fmax_num(fmax_num(s[kb][0], s[kb][1]), fmax_num(s[kb][2], s[kb][3]));
-#pragma unroll
-    for (int w = NB / 2; w >= 1; w /= 2)
-#pragma unroll
-        for (int kb = 0; kb < w; ++kb) v[kb] = fmax_num(v[kb], v[kb + w]);
-    return v[0];
+    static_assert(NB == 2 || NB == 4, "tree shapes for 8 and 16 values");
+    if constexpr (NB == 4) {  // 16 values: 5 + 2 three-input maxima and one pair
+        const float a0 = max3(s[0][0], s[0][1], s[0][2]), a1 = max3(s[0][3], s[1][0], s[1][1]);
+        const float a2 = max3(s[1][2], s[1][3], s[2][0]), a3 = max3(s[2][1], s[2][2], s[2][3]);
+        const float a4 = max3(s[3][0], s[3][1], s[3][2]);
+        return fmax_num(max3(a0, a1, a2), max3(a3, a4, s[3][3]));
+    } else {  // 8 values: two three-input maxima and one more over the rest
+        const float a0 = max3(s[0][0], s[0][1], s[0][2]), a1 = max3(s[0][3], s[1][0], s[1][1]);
+        return max3(a0, a1, fmax_num(s[1][2], s[1][3]));
+    }
 }
 template <int NB>
 __device__ __forceinline__ float tree_sum(const f32x4 (&s)[NB]) {
@@ -1194,10 +1198,9 @@ hipError_t launch_few(const KArgs& a, int head_dim, int rb, hipStream_t s) {
         if (rb == 1) hipLaunchKernelGGL((few_kernel<64, 1>), g, b, 0, s, a);
         else if (rb == 2) hipLaunchKernelGGL((few_kernel<64, 2>), g, b, 0, s, a);
         else hipLaunchKernelGGL((few_kernel<64, 4>), g, b, 0, s, a);
-    } else {
+    } else {  // the planner gives d = 128 units at most 32 rows
         if (rb == 1) hipLaunchKernelGGL((few_kernel<128, 1>), g, b, 0, s, a);
-        else if (rb == 2) hipLaunchKernelGGL((few_kernel<128, 2>), g, b, 0, s, a);
-        else hipLaunchKernelGGL((few_kernel<128, 4>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((few_kernel<128, 2>), g, b, 0, s, a);
     }
     return hipGetLastError();
 }

@@ -318,13 +318,20 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         const int32_t own0 = member ? groups[group_of[r]].prefix_len : 0;
         if (member && v.hi[s.q_len - 1] <= own0) continue;  // the prefix is all it sees
         if (R <= kDecodeMaxRows) {
+            // at d = 128 a unit holds at most 32 rows: the 64-row instance of
+            // the few-row kernel does not fit its registers
+            const int32_t span = P.head_dim == 128 ? 32 : kDecodeMaxRows;
             for (int32_t kvh = 0; kvh < P.num_kv_heads; ++kvh) {
-                Unit u{r, kvh, 0, (int32_t)R, member ? own0 : align_down16(v.lo[0]), v.hi[s.q_len - 1], 0};
-                u.cost = (int64_t)(u.k_end - u.k_begin);
-                u.partial = member;
-                few_units.push_back(u);
+                for (int32_t rr0 = 0; rr0 < R; rr0 += span) {
+                    const int32_t nr = std::min<int32_t>(span, (int32_t)R - rr0);
+                    const int32_t q0 = rr0 / G, q1 = (rr0 + nr - 1) / G;
+                    Unit u{r, kvh, rr0, nr, member ? own0 : align_down16(v.lo[q0]), v.hi[q1], 0};
+                    u.cost = (int64_t)(u.k_end - u.k_begin);
+                    u.partial = member;
+                    few_units.push_back(u);
+                    plan.decode_rb = std::max<int32_t>(plan.decode_rb, nr <= 16 ? 1 : nr <= 32 ? 2 : 4);
+                }
             }
-            plan.decode_rb = std::max<int32_t>(plan.decode_rb, R <= 16 ? 1 : R <= 32 ? 2 : 4);
         } else {
             // one unit per row tile, shared by every query head
             for (int32_t row0 = 0; row0 < s.q_len; row0 += kTileRows) {

@@ -372,3 +372,17 @@ def test_cascade_rejects_bad_groups():
                   f.block_table.shape[1], f.num_pages, f.sm_scale, attn.FLAG_HOST_ONLY,
                   prefix_groups=[([0, 1], 16)]).destroy()
     assert ei.value.code == attn.ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("d,limit", [(128, 32), (64, 64)])
+def test_few_row_items_hold_at_most_32_rows_at_d128(d, limit):
+    """At d = 128 a decode-like request with 33..64 (query row, head) rows is
+    cut into units of at most 32 rows (the 64-row few-row instance does not
+    fit its registers there); at d = 64 one unit takes all 64."""
+    b = W.mixed(seed=3, hq=8, hkv=2, d=d)
+    G = b.num_qo_heads // b.num_kv_heads
+    assert 64 in {int(x) * G for x in b.seqs[:, 0]}
+    pl = plan_for(b, attn.FLAG_HOST_ONLY)
+    rows = [int(x[3]) for x in pl.items(1)]
+    assert rows and max(rows) == limit
+    pl.destroy()
