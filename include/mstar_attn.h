@@ -279,6 +279,8 @@ int mstar_attn_plan_cascade_order(const mstar_plan_t* plan, int32_t* pairs, int6
  *   mstar_attn_plan; the device is the calling thread's current one) and
  *   returns at once, unless `depth` plans are outstanding, in which case it
  *   waits until one is taken.  Plans are built in submission order.
+ * mstar_planner_submit_cascade: the same for mstar_attn_plan_cascade (shared-
+ *   prefix groups, copied like the descriptors).
  * mstar_planner_take: waits for the oldest outstanding plan, makes `stream`
  *   wait (on the device, no host sync) for its upload, and returns it; the
  *   caller owns it (mstar_attn_plan_destroy).  A planning error is returned
@@ -293,6 +295,10 @@ int mstar_planner_create(int32_t depth, mstar_planner_t** out);
 int mstar_planner_submit(mstar_planner_t* planner, const mstar_attn_params* params, const mstar_seq_desc* seqs,
                          const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segments,
                          int32_t num_segs);
+int mstar_planner_submit_cascade(mstar_planner_t* planner, const mstar_attn_params* params,
+                                 const mstar_seq_desc* seqs, const mstar_mask_spec* masks, int32_t num_seqs,
+                                 const mstar_segment* segments, int32_t num_segs, const mstar_prefix_group* groups,
+                                 int32_t num_groups, const int32_t* members, int32_t num_members);
 int mstar_planner_take(mstar_planner_t* planner, void* stream, mstar_plan_t** out);
 int mstar_attn_plan_wait(const mstar_plan_t* plan, void* stream);
 void mstar_planner_destroy(mstar_planner_t* planner);

@@ -48,6 +48,7 @@ EXPORTS = [
     "mstar_kv_append",
     "mstar_planner_create",
     "mstar_planner_submit",
+    "mstar_planner_submit_cascade",
     "mstar_planner_take",
     "mstar_attn_plan_wait",
     "mstar_planner_destroy",
@@ -137,6 +138,10 @@ def lib() -> ctypes.CDLL:
     L.mstar_planner_submit.argtypes = [vp, ctypes.POINTER(Params), ctypes.POINTER(SeqDesc), ctypes.POINTER(MaskSpec),
                                        i32, ctypes.POINTER(Segment), i32]
     L.mstar_planner_submit.restype = ctypes.c_int
+    L.mstar_planner_submit_cascade.argtypes = [vp, ctypes.POINTER(Params), ctypes.POINTER(SeqDesc),
+                                               ctypes.POINTER(MaskSpec), i32, ctypes.POINTER(Segment), i32,
+                                               ctypes.POINTER(PrefixGroup), i32, ctypes.POINTER(i32), i32]
+    L.mstar_planner_submit_cascade.restype = ctypes.c_int
     L.mstar_planner_take.argtypes = [vp, vp, ctypes.POINTER(vp)]
     L.mstar_planner_take.restype = ctypes.c_int
     L.mstar_attn_plan_wait.argtypes = [vp, vp]
@@ -258,6 +263,18 @@ def _descriptors(num_qo_heads, num_kv_heads, head_dim, dtype, seqs, masks, segme
     return p, s_arr, n, m_arr, g_arr, ns, total_q
 
 
+def _groups(prefix_groups):
+    """``[(member request indices, prefix_len), ...]`` -> mstar_prefix_group array and member array."""
+    members = [int(r) for mem, _ in prefix_groups for r in mem]
+    gr = (PrefixGroup * len(prefix_groups))()
+    k = 0
+    for i, (mem, plen) in enumerate(prefix_groups):
+        gr[i].member_begin, gr[i].member_count, gr[i].prefix_len = k, len(mem), int(plen)
+        k += len(mem)
+    mem_arr = (ctypes.c_int32 * max(len(members), 1))(*members)
+    return gr, len(prefix_groups), mem_arr, len(members)
+
+
 def plan(num_qo_heads: int, num_kv_heads: int, head_dim: int, dtype: str, seqs, masks, segments,
          max_blocks_per_seq: int, num_pages: int, sm_scale: Optional[float] = None, flags: int = 0,
          stream=None, page_size: int = 16, prefix_groups=None) -> Plan:
@@ -271,16 +288,9 @@ def plan(num_qo_heads: int, num_kv_heads: int, head_dim: int, dtype: str, seqs, 
     h = ctypes.c_void_p(None)
     stream_h = None if flags & FLAG_HOST_ONLY else _stream_handle(stream)
     if prefix_groups:
-        # prefix_groups: [(member request indices, prefix_len), ...]
-        members = [int(r) for mem, _ in prefix_groups for r in mem]
-        gr = (PrefixGroup * len(prefix_groups))()
-        k = 0
-        for i, (mem, plen) in enumerate(prefix_groups):
-            gr[i].member_begin, gr[i].member_count, gr[i].prefix_len = k, len(mem), int(plen)
-            k += len(mem)
-        mem_arr = (ctypes.c_int32 * max(len(members), 1))(*members)
-        _check_rc(lib().mstar_attn_plan_cascade(ctypes.byref(p), s_arr, m_arr, n, g_arr, ns, gr, len(prefix_groups),
-                                                mem_arr, len(members), stream_h, ctypes.byref(h)))
+        gr, ng, mem_arr, nm = _groups(prefix_groups)
+        _check_rc(lib().mstar_attn_plan_cascade(ctypes.byref(p), s_arr, m_arr, n, g_arr, ns, gr, ng, mem_arr, nm,
+                                                stream_h, ctypes.byref(h)))
     else:
         _check_rc(lib().mstar_attn_plan(ctypes.byref(p), s_arr, m_arr, n, g_arr, ns, stream_h, ctypes.byref(h)))
     return Plan(h.value, p, n, total_q)
@@ -290,7 +300,8 @@ class AsyncPlanner:
     """``mstar_planner_*``: plans built in submission order on a native worker
     thread with its own HIP stream, at most ``depth`` outstanding (double
     buffering with the default 2).  :meth:`submit` takes the arguments of
-    :func:`plan` (without ``stream``); :meth:`take` returns the oldest plan
+    :func:`plan` (without ``stream``; with ``prefix_groups`` it is
+    ``mstar_planner_submit_cascade``); :meth:`take` returns the oldest plan
     after making ``stream`` wait for its upload."""
 
     def __init__(self, depth: int = 2):
@@ -300,11 +311,16 @@ class AsyncPlanner:
         self._pending = []
 
     def submit(self, num_qo_heads, num_kv_heads, head_dim, dtype, seqs, masks, segments, max_blocks_per_seq,
-               num_pages, sm_scale=None, flags=0, page_size=16):
+               num_pages, sm_scale=None, flags=0, page_size=16, prefix_groups=None):
         p, s_arr, n, m_arr, g_arr, ns, total_q = _descriptors(num_qo_heads, num_kv_heads, head_dim, dtype, seqs,
                                                               masks, segments, max_blocks_per_seq, num_pages,
                                                               sm_scale, flags, page_size)
-        _check_rc(lib().mstar_planner_submit(self._h, ctypes.byref(p), s_arr, m_arr, n, g_arr, ns))
+        if prefix_groups:
+            gr, ng, mem_arr, nm = _groups(prefix_groups)
+            _check_rc(lib().mstar_planner_submit_cascade(self._h, ctypes.byref(p), s_arr, m_arr, n, g_arr, ns, gr, ng,
+                                                         mem_arr, nm))
+        else:
+            _check_rc(lib().mstar_planner_submit(self._h, ctypes.byref(p), s_arr, m_arr, n, g_arr, ns))
         self._pending.append((p, n, total_q))
 
     def take(self, stream=None) -> Plan:

@@ -426,6 +426,8 @@ struct mstar_planner {
         std::vector<mstar_seq_desc> seqs;
         std::vector<mstar_mask_spec> masks;
         std::vector<mstar_segment> segs;
+        std::vector<mstar_prefix_group> groups;  // empty: a plain plan
+        std::vector<int32_t> members;
         int device = 0;
     };
     struct Done {
@@ -474,8 +476,10 @@ struct mstar_planner {
                 s = stream;
             }
             if (d.rc == MSTAR_OK) {
-                d.rc = mstar_attn_plan(&job.p, job.seqs.data(), job.masks.data(), (int32_t)job.seqs.size(),
-                                       job.segs.data(), (int32_t)job.segs.size(), s, &d.plan);
+                d.rc = mstar_attn_plan_cascade(&job.p, job.seqs.data(), job.masks.data(), (int32_t)job.seqs.size(),
+                                               job.segs.data(), (int32_t)job.segs.size(), job.groups.data(),
+                                               (int32_t)job.groups.size(), job.members.data(),
+                                               (int32_t)job.members.size(), s, &d.plan);
                 if (d.rc != MSTAR_OK) {
                     d.err = mstar_last_error();
                 } else if (!host_only) {
@@ -519,12 +523,16 @@ MSTAR_EXPORT int mstar_planner_create(int32_t depth, mstar_planner_t** out) {
     return MSTAR_OK;
 }
 
-MSTAR_EXPORT int mstar_planner_submit(mstar_planner_t* planner, const mstar_attn_params* params,
-                                      const mstar_seq_desc* seqs, const mstar_mask_spec* masks, int32_t num_seqs,
-                                      const mstar_segment* segments, int32_t num_segs) {
+MSTAR_EXPORT int mstar_planner_submit_cascade(mstar_planner_t* planner, const mstar_attn_params* params,
+                                              const mstar_seq_desc* seqs, const mstar_mask_spec* masks,
+                                              int32_t num_seqs, const mstar_segment* segments, int32_t num_segs,
+                                              const mstar_prefix_group* groups, int32_t num_groups,
+                                              const int32_t* members, int32_t num_members) {
     if (!planner || !params) return fail(MSTAR_ERR_INVALID_ARG, "planner or params is NULL");
-    if (num_seqs < 0 || num_segs < 0) return fail(MSTAR_ERR_INVALID_ARG, "negative count");
-    if ((num_seqs > 0 && (!seqs || !masks)) || (num_segs > 0 && !segments))
+    if (num_seqs < 0 || num_segs < 0 || num_groups < 0 || num_members < 0)
+        return fail(MSTAR_ERR_INVALID_ARG, "negative count");
+    if ((num_seqs > 0 && (!seqs || !masks)) || (num_segs > 0 && !segments) || (num_groups > 0 && !groups) ||
+        (num_members > 0 && !members))
         return fail(MSTAR_ERR_INVALID_ARG, "descriptor pointer is NULL");
     mstar_planner::Job job;
     try {
@@ -532,6 +540,8 @@ MSTAR_EXPORT int mstar_planner_submit(mstar_planner_t* planner, const mstar_attn
         job.seqs.assign(seqs, seqs + num_seqs);
         job.masks.assign(masks, masks + num_seqs);
         job.segs.assign(segments, segments + num_segs);
+        job.groups.assign(groups, groups + num_groups);
+        job.members.assign(members, members + num_members);
     } catch (const std::bad_alloc&) {
         return fail(MSTAR_ERR_NOMEM, "host allocation failed");
     }
@@ -548,6 +558,13 @@ MSTAR_EXPORT int mstar_planner_submit(mstar_planner_t* planner, const mstar_attn
     }
     planner->cv_work.notify_one();
     return MSTAR_OK;
+}
+
+MSTAR_EXPORT int mstar_planner_submit(mstar_planner_t* planner, const mstar_attn_params* params,
+                                      const mstar_seq_desc* seqs, const mstar_mask_spec* masks, int32_t num_seqs,
+                                      const mstar_segment* segments, int32_t num_segs) {
+    return mstar_planner_submit_cascade(planner, params, seqs, masks, num_seqs, segments, num_segs, nullptr, 0,
+                                        nullptr, 0);
 }
 
 MSTAR_EXPORT int mstar_planner_take(mstar_planner_t* planner, void* stream, mstar_plan_t** out) {

@@ -121,3 +121,24 @@ def test_close_with_untaken_plans_releases_them():
     for n in ("decode_bf16", "mixed", "rollout_bf16"):
         ap.submit(*_args(W.reduced(n)))
     ap.close()  # joins the worker and destroys the three plans
+
+
+@pytest.mark.parametrize("name", ["shared_prefix_decode_bf16", "rollout_bf16", "mixed"])
+def test_cascade_plans_through_the_planner_equal_synchronous_ones(name):
+    """mstar_planner_submit_cascade builds the same plan as mstar_attn_plan_cascade."""
+    b = W.reduced(name)
+    ap = attn.AsyncPlanner(depth=2)
+    for flags in (attn.FLAG_HOST_ONLY, attn.FLAG_HOST_ONLY | attn.FLAG_CASCADE_ALL):
+        ap.submit(*_args(b, flags), prefix_groups=b.prefix_groups)
+        got = ap.take()
+        ref = plan_for(b, flags, cascade=True)
+        _same(got, ref)
+        for kind in (4, 5):
+            assert np.array_equal(got.items(kind), ref.items(kind))
+        assert np.array_equal(got.tile_order(cascade=True), ref.tile_order(cascade=True))
+        got.destroy()
+        ref.destroy()
+    with pytest.raises(attn.MStarError):  # a bad group surfaces at take
+        ap.submit(*_args(b), prefix_groups=[([0, 0], 64)])
+        ap.take()
+    ap.close()

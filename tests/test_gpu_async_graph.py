@@ -1,8 +1,8 @@
 """GPU tests of asynchronous planning and graph capture: a serving loop that
 builds each step's plan on the planner's thread and stream while the previous
-step runs (results against the oracle), and kv_append + fwd captured in a HIP
-graph, replayed with eager work in between, every replay bitwise equal to the
-eager call."""
+step runs (results against the oracle; plain and shared-prefix cascade plans),
+and kv_append + fwd captured in a HIP graph, replayed with eager work in
+between, every replay bitwise equal to the eager call."""
 import numpy as np
 import pytest
 
@@ -28,14 +28,25 @@ def test_async_planner_serving_loop_against_oracle():
     import torch
 
     steps = [W.reduced(n, seed=s) for s, n in enumerate(
-        ["decode_bf16", "mixed", "rollout_bf16", "stream_window_bf16", "cfg_labels_bf16", "text_latent_bf16"])]
+        ["decode_bf16", "mixed", "rollout_bf16", "stream_window_bf16", "cfg_labels_bf16", "text_latent_bf16",
+         "shared_prefix_decode_bf16", "rollout_bf16"])]
+    # the last two steps are planned as shared-prefix cascades (the second with every member in)
+    cascade = {6: 0, 7: attn.FLAG_CASCADE_ALL}
+
+    def submit(i):
+        b = steps[i]
+        if i in cascade:
+            ap.submit(*_args(b, cascade[i]), prefix_groups=b.prefix_groups)
+        else:
+            ap.submit(*_args(b))
+
     stream = torch.cuda.current_stream()
     ap = attn.AsyncPlanner(depth=2)
-    ap.submit(*_args(steps[0]))
+    submit(0)
     for i, b in enumerate(steps):
         t = W.make_tensors_torch(b, DEV)
         if i + 1 < len(steps):
-            ap.submit(*_args(steps[i + 1]))  # planned on the worker while this step runs
+            submit(i + 1)  # planned on the worker while this step runs
         pl = ap.take(stream)                 # the stream waits for the upload on the device
         out = torch.empty_like(t["q"])
         lse = torch.empty(t["q"].shape[:2], dtype=torch.float32, device=DEV)
@@ -51,8 +62,10 @@ def test_async_planner_serving_loop_against_oracle():
     ap.close()
 
 
-@pytest.mark.parametrize("name,flags", [("mixed", 0), ("decode_bf16", attn.FLAG_FORCE_SPLIT), ("rollout_bf16", 0)])
-def test_append_and_fwd_captured_in_a_graph_replay_bitwise(name, flags):
+@pytest.mark.parametrize("name,flags,cascade", [("mixed", 0, False), ("decode_bf16", attn.FLAG_FORCE_SPLIT, False),
+                                                ("rollout_bf16", 0, False), ("shared_prefix_decode_bf16", 0, True),
+                                                ("rollout_bf16", attn.FLAG_CASCADE_ALL, True)])
+def test_append_and_fwd_captured_in_a_graph_replay_bitwise(name, flags, cascade):
     import torch
 
     b = W.reduced(name)
@@ -61,7 +74,7 @@ def test_append_and_fwd_captured_in_a_graph_replay_bitwise(name, flags):
     g0.manual_seed(5)
     kn = torch.randn((b.total_q, b.num_kv_heads, b.head_dim), generator=g0, device=DEV).to(torch.bfloat16)
     vn = torch.randn((b.total_q, b.num_kv_heads, b.head_dim), generator=g0, device=DEV).to(torch.bfloat16)
-    pl = plan_for(b, flags)
+    pl = plan_for(b, flags, cascade=cascade)
     bt = torch.from_numpy(np.ascontiguousarray(b.block_table)).to(DEV)
     ws = attn.workspace(pl, DEV)
     out = torch.empty_like(t["q"])
