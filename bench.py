@@ -42,11 +42,11 @@ PEAK_BF16_TFLOPS = 2516.6   # dense MFMA: 256 CU x 2.4 GHz x 4096 FLOP/clk
 PEAK_FP32_TFLOPS = 157.3
 BOUND = {"tiny_causal_f32": "alu", "decode_bf16": "hbm", "text_latent_bf16": "mfma",
          "stream_window_bf16": "hbm", "rollout_bf16": "mfma", "cfg_labels_bf16": "mfma",
-         "shared_prefix_decode_bf16": "hbm"}
+         "shared_prefix_decode_bf16": "hbm", "serving_mix_bf16": "mfma"}
 # kernel classes of mstar_attn_fwd_timed: 0 multi-row tiles, 1 few-row items, 2 fp32, 3 merge, 4 cascade
 KERNEL_NAMES = ["tile_kernel", "few_kernel", "f32_kernel", "merge_kernel", "cascade_kernel"]
 DOMINANT = {"tiny_causal_f32": 2, "decode_bf16": 1, "text_latent_bf16": 0, "stream_window_bf16": 1,
-            "rollout_bf16": 0, "cfg_labels_bf16": 0, "shared_prefix_decode_bf16": 1}
+            "rollout_bf16": 0, "cfg_labels_bf16": 0, "shared_prefix_decode_bf16": 1, "serving_mix_bf16": 0}
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_12688_amd", "csrc", "kernels.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -235,6 +235,8 @@ def main():
     ap.add_argument("--workload", default="decode_bf16", choices=sorted(BOUND))
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--serial", action="store_true",
+                    help="plan with MSTAR_FLAG_SERIAL: every kernel on the caller's stream, none beside another")
     ap.add_argument("--cascade", action="store_true",
                     help="plan with the workload's shared-prefix groups (mstar_attn_plan_cascade); the roofline "
                          "then divides by the summed time of every kernel of the step")
@@ -284,8 +286,8 @@ def main():
 
     def make_plan():
         return attn.plan(b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, b.seqs, b.masks, b.segments,
-                         b.block_table.shape[1], b.num_pages, b.sm_scale, 0, stream,
-                         prefix_groups=b.prefix_groups if args.cascade else None)
+                         b.block_table.shape[1], b.num_pages, b.sm_scale, attn.FLAG_SERIAL if args.serial else 0,
+                         stream, prefix_groups=b.prefix_groups if args.cascade else None)
     # the first plan of a process includes one-time set-up (pinned staging, HIP
     # context work); the reported planning time is that of a second plan
     pl_first = make_plan()
@@ -337,9 +339,14 @@ def main():
                 arr[side][k] = evs[i][side][k].cuda_event
         ev_arrays[i] = arr
 
+    # the whole call on the caller's stream (all kernels, forks and joins included)
+    span = {i: [torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for i in sampled}
+
     def step(i, timed=False):
         if timed and i in ev_arrays:
+            span[i][0].record(stream)
             rc = L.mstar_attn_fwd_timed(*calls[i % n_rot], ev_arrays[i][0], ev_arrays[i][1])
+            span[i][1].record(stream)
         else:
             rc = L.mstar_attn_fwd(*calls[i % n_rot])
         if rc != 0:
@@ -356,9 +363,11 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / K
     per_kernel = {KERNEL_NAMES[k]: np.array([evs[i][0][k].elapsed_time(evs[i][1][k]) for i in sampled])
                   for k in launched}
-    if args.cascade:  # the step's work is spread over several kernels: their summed time
-        kernel_ms = sum(per_kernel.values())
-        dominant = "+".join(KERNEL_NAMES[k] for k in launched)
+    span_ms = np.array([span[i][0].elapsed_time(span[i][1]) for i in sampled])
+    if len([k for k in launched if k in (0, 1, 4)]) > 1:
+        # the step's work is spread over several kernels, some side by side: the call's span
+        kernel_ms = span_ms
+        dominant = "call(" + "+".join(KERNEL_NAMES[k] for k in launched) + ")"
     else:
         kernel_ms = per_kernel[KERNEL_NAMES[DOMINANT[args.workload]]]
         dominant = KERNEL_NAMES[DOMINANT[args.workload]]
@@ -396,9 +405,11 @@ def main():
                      "frac": round(achieved / peak, 4), "traffic": traffic},
         "tflops": round(tflops, 3), "kv_gbps": round(gbps, 3),
         "tflops_frac_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4), "kv_gbps_frac_hbm_peak": round(gbps / PEAK_HBM_GBS, 4),
-        "dominant_kernel": dominant, "cascade": bool(args.cascade),
+        "dominant_kernel": dominant, "cascade": bool(args.cascade), "serial": bool(args.serial),
         "kernel_ms": {name: {"mean": round(float(v.mean()), 5), "median": round(float(np.median(v)), 5),
                              "p95": round(float(np.percentile(v, 95)), 5)} for name, v in per_kernel.items()},
+        "call_ms": {"mean": round(float(span_ms.mean()), 5), "median": round(float(np.median(span_ms)), 5),
+                    "p95": round(float(np.percentile(span_ms, 95)), 5)},
         "useful_flop": flop, "kv_bytes": nbytes, "plan_host_us": round(st["plan_host_us"], 1),
         "plan_host_us_first_call": round(plan_first_us, 1), "event_sampled_steps": len(sampled),
         "plan": {k: st[k] for k in ("prefill_items", "decode_items", "f32_items", "merge_rows", "partial_slots")},

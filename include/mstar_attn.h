@@ -68,6 +68,8 @@ extern "C" {
                                      rejects such a plan                                         */
 #define MSTAR_FLAG_CASCADE_ALL 8u /* mstar_attn_plan_cascade: every group member joins the cascade,
                                      not only the decode-like ones                               */
+#define MSTAR_FLAG_SERIAL 16u     /* fwd runs every kernel on the caller's stream, one after the
+                                     other (no side stream)                                      */
 
 /* Bits of the sticky device error word (see mstar_attn_check). */
 #define MSTAR_DEVERR_PAGE_RANGE 1 /* a block-table entry was outside [0, num_pages) */
@@ -195,11 +197,19 @@ size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan);
  * memory, written for every row of every request (rows of no request are
  * untouched).  workspace: caller-owned device memory of at least
  * mstar_attn_workspace_bytes(plan) bytes (may be NULL if that is 0); fwd
- * overwrites it.  Enqueues at most four kernels (multi-row tiles, few-row
- * items, fp32 items, then the merge of split key ranges); no allocation, no host
- * synchronization and no host reads, so the call may be captured in a HIP
- * graph.  The same plan may run with any tensors of the planned shapes.  Two
- * fwd calls that overlap in time must use different workspaces.  Block-table
+ * overwrites it.  Enqueues at most four kernels (multi-row tiles or cascade
+ * items, few-row items, fp32 items, then the merge of split key ranges); no
+ * allocation, no host synchronization and no host reads, so the call may be
+ * captured in a HIP graph.  When a plan has both multi-row tile items and
+ * few-row items, the few-row kernel runs beside the tile kernel on a side stream of the
+ * calling thread (default priority, created by the thread's first such call
+ * outside graph capture and kept until the process ends; inside a capture
+ * before it exists the kernels run one after the other): `stream` forks to it
+ * and joins back before the merge through two events of the plan, so calls
+ * with one plan must not overlap in time (MSTAR_FLAG_SERIAL turns this off).
+ * The same plan may run with any
+ * tensors of the planned shapes.  Two fwd calls that overlap in time must use
+ * different workspaces.  Block-table
  * entries outside [0, num_pages) are never dereferenced: they read as zeros
  * and set MSTAR_DEVERR_PAGE_RANGE in the plan's device error word.
  * Errors: INVALID_ARG (null tensor pointer, misaligned pointer), WORKSPACE,
@@ -209,8 +219,9 @@ int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const void* k_pages,
                    void* workspace, size_t workspace_bytes, void* stream);
 
 /* mstar_attn_fwd, additionally recording caller-created HIP events
- * (hipEvent_t) on `stream` right before and right after each kernel it
- * enqueues: index 0 = multi-row tile kernel, 1 = few-row kernel, 2 = fp32
+ * (hipEvent_t) right before and right after each kernel it enqueues, on the
+ * stream that kernel runs on (`stream`, or the side stream for a few-row
+ * kernel beside multi-row work): index 0 = multi-row tile kernel, 1 = few-row kernel, 2 = fp32
  * kernel, 3 = merge kernel, 4 = shared-prefix cascade kernel (arrays of 5
  * entries).  Either array, and any entry, may be NULL; events
  * of kernels the plan does not launch are left untouched.  For per-kernel

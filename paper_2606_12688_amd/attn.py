@@ -30,7 +30,7 @@ ERR_NOMEM = -5
 
 SEG_CAUSAL, SEG_FULL, SEG_BLOCKS = 0, 1, 2
 DTYPE_F32, DTYPE_BF16 = 0, 1
-FLAG_FORCE_SPLIT, FLAG_NO_SPLIT, FLAG_HOST_ONLY, FLAG_CASCADE_ALL = 1, 2, 4, 8
+FLAG_FORCE_SPLIT, FLAG_NO_SPLIT, FLAG_HOST_ONLY, FLAG_CASCADE_ALL, FLAG_SERIAL = 1, 2, 4, 8, 16
 DEVERR_PAGE_RANGE = 1
 
 EXPORTS = [

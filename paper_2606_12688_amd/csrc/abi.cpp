@@ -28,6 +28,10 @@ struct mstar_plan {
     size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_order = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_append = 0, off_casc = 0, off_casc_rows = 0, off_casc_order = 0, off_err = 0;
     double plan_us = 0.0;
     hipEvent_t ready = nullptr;  // recorded after the upload by the async planner
+    // A plan with both tile and few-row items runs the few-row kernel on a
+    // side stream beside the tile kernel: the caller's stream forks at `fork`
+    // and joins at `join` before the merge.
+    hipEvent_t fork = nullptr, join = nullptr;
 };
 
 namespace {
@@ -44,6 +48,24 @@ int hip_fail(hipError_t e, const char* what) {
 }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// The calling thread's side stream on the current device (default priority,
+// non-blocking), created on first use and kept until the process ends; one per
+// thread, so that work forked by different threads (or captured into a graph
+// by one of them) never shares a stream.  It is not created while `main` is
+// being captured into a graph.  nullptr if it cannot be had.
+hipStream_t side_stream(hipStream_t main) {
+    constexpr int kMaxDevices = 64;
+    thread_local hipStream_t streams[kMaxDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    if (!streams[dev]) {
+        hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(main, &st) != hipSuccess || st != hipStreamCaptureStatusNone) return nullptr;
+        if (hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking) != hipSuccess) streams[dev] = nullptr;
+    }
+    return streams[dev];
+}
 
 template <typename T>
 size_t put(unsigned char* blob, size_t off, const std::vector<T>& v) {
@@ -130,7 +152,16 @@ static int plan_impl(const mstar_attn_params* params, const mstar_seq_desc* seqs
         }
         e = hipMemcpyAsync(plan->dev, plan->pinned, plan->bytes, hipMemcpyHostToDevice,
                            static_cast<hipStream_t>(upload_stream));
+        // the few-row kernel goes beside the tile kernel (prefill work), not
+        // beside the cascade kernel, whose L2-fed prefix tiles and the few-row
+        // kernel's HBM stream slow each other down more than they overlap
+        if (e == hipSuccess && !h.tiles.empty() && !h.few.empty() && !(p.flags & MSTAR_FLAG_SERIAL)) {
+            e = hipEventCreateWithFlags(&plan->fork, hipEventDisableTiming);
+            if (e == hipSuccess) e = hipEventCreateWithFlags(&plan->join, hipEventDisableTiming);
+        }
         if (e != hipSuccess) {
+            if (plan->fork) (void)hipEventDestroy(plan->fork);
+            if (plan->join) (void)hipEventDestroy(plan->join);
             (void)hipFree(plan->dev);
             (void)hipHostFree(plan->pinned);
             delete plan;
@@ -216,13 +247,34 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
     hipStream_t s = static_cast<hipStream_t>(stream);
 
     hipError_t e;
-    // optional HIP events around kernel class k (0 tiles, 1 few-row, 2 fp32, 3 merge, 4 cascade)
+    // The few-row kernel runs on the thread's side stream when the plan also
+    // has tile work: it streams K/V from HBM while the tile kernel keeps the
+    // matrix units busy.  Both write disjoint outputs and partial slots; the
+    // merge waits for both.
+    hipStream_t side = plan->fork ? side_stream(s) : nullptr;
+    if (side) {
+        if ((e = hipEventRecord(plan->fork, s)) != hipSuccess) return hip_fail(e, "hipEventRecord(fork)");
+        if ((e = hipStreamWaitEvent(side, plan->fork, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(fork)");
+    }
+    hipStream_t s_few = side ? side : s;
+    // optional HIP events around kernel class k (0 tiles, 1 few-row, 2 fp32, 3 merge, 4 cascade),
+    // recorded on the stream that kernel runs on
     auto mark = [&](void* const* evs, int k) -> hipError_t {
         if (!evs || !evs[k]) return hipSuccess;
-        return hipEventRecord(static_cast<hipEvent_t>(evs[k]), s);
+        return hipEventRecord(static_cast<hipEvent_t>(evs[k]), k == 1 ? s_few : s);
     };
 #define MSTAR_MARK(evs, k) \
     if ((e = mark(evs, k)) != hipSuccess) return hip_fail(e, "hipEventRecord")
+    if (!h.few.empty()) {
+        a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_few);
+        a.n_items = (int32_t)h.few.size();
+        MSTAR_MARK(events_before, 1);
+        if ((e = mstar::launch_few(a, D, h.decode_rb, s_few)) != hipSuccess) return hip_fail(e, "few-row kernel launch");
+        MSTAR_MARK(events_after, 1);
+    }
+    if (side) {
+        if ((e = hipEventRecord(plan->join, side)) != hipSuccess) return hip_fail(e, "hipEventRecord(join)");
+    }
     if (!h.tiles.empty()) {
         a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_tiles);
         a.n_items = (int32_t)h.tiles.size();
@@ -242,12 +294,8 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
         if ((e = mstar::launch_cascade(a, D, s)) != hipSuccess) return hip_fail(e, "cascade kernel launch");
         MSTAR_MARK(events_after, 4);
     }
-    if (!h.few.empty()) {
-        a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_few);
-        a.n_items = (int32_t)h.few.size();
-        MSTAR_MARK(events_before, 1);
-        if ((e = mstar::launch_few(a, D, h.decode_rb, s)) != hipSuccess) return hip_fail(e, "few-row kernel launch");
-        MSTAR_MARK(events_after, 1);
+    if (side) {
+        if ((e = hipStreamWaitEvent(s, plan->join, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(join)");
     }
     if (!h.f32.empty()) {
         a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_f32);
@@ -406,6 +454,8 @@ MSTAR_EXPORT int mstar_attn_plan_cascade_order(const mstar_plan_t* plan, int32_t
 MSTAR_EXPORT void mstar_attn_plan_destroy(mstar_plan_t* plan) {
     if (!plan) return;
     if (plan->ready) (void)hipEventDestroy(plan->ready);
+    if (plan->fork) (void)hipEventDestroy(plan->fork);
+    if (plan->join) (void)hipEventDestroy(plan->join);
     if (plan->dev) (void)hipFree(plan->dev);
     if (plan->pinned) (void)hipHostFree(plan->pinned);
     delete plan;

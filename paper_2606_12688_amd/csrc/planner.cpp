@@ -164,7 +164,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         err = "FORCE_SPLIT and NO_SPLIT are exclusive";
         return MSTAR_ERR_INVALID_ARG;
     }
-    if (P.flags & ~(MSTAR_FLAG_FORCE_SPLIT | MSTAR_FLAG_NO_SPLIT | MSTAR_FLAG_CASCADE_ALL)) {
+    if (P.flags & ~(MSTAR_FLAG_FORCE_SPLIT | MSTAR_FLAG_NO_SPLIT | MSTAR_FLAG_CASCADE_ALL | MSTAR_FLAG_SERIAL)) {
         err = "unknown flag";
         return MSTAR_ERR_INVALID_ARG;
     }

@@ -26,7 +26,7 @@ def test_library_exports_every_declared_symbol():
 
 
 WORKLOADS = ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16", "rollout_bf16",
-             "cfg_labels_bf16", "mixed"]
+             "cfg_labels_bf16", "serving_mix_bf16", "mixed"]
 
 
 def _coverage(b, flags):
@@ -254,7 +254,7 @@ def test_cascade_launch_order_spreads_one_group_over_every_xcd():
     pl.destroy()
 
 
-CASCADE = ["rollout_bf16", "cfg_labels_bf16", "mixed", "shared_prefix_decode_bf16"]
+CASCADE = ["rollout_bf16", "cfg_labels_bf16", "mixed", "shared_prefix_decode_bf16", "serving_mix_bf16"]
 
 
 @pytest.mark.parametrize("name", CASCADE)

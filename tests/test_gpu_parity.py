@@ -38,8 +38,8 @@ def _oracle(b, t):
 
 
 REDUCED = ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16", "rollout_bf16",
-           "cfg_labels_bf16", "shared_prefix_decode_bf16", "mixed"]
-CASCADE = ["rollout_bf16", "cfg_labels_bf16", "shared_prefix_decode_bf16", "mixed"]
+           "cfg_labels_bf16", "shared_prefix_decode_bf16", "serving_mix_bf16", "mixed"]
+CASCADE = ["rollout_bf16", "cfg_labels_bf16", "shared_prefix_decode_bf16", "serving_mix_bf16", "mixed"]
 FLAGS = {"auto": 0, "force_split": attn.FLAG_FORCE_SPLIT, "no_split": attn.FLAG_NO_SPLIT}
 
 
@@ -65,6 +65,27 @@ def test_cascade_parity(name, flag):
     for extra, tag in ((attn.FLAG_CASCADE_ALL, "all"), (0, "default")):
         out, lse = run_gpu(b, t, FLAGS[flag] | extra, cascade=True)
         _compare(b, out, lse, ro, rl, f"{name}/cascade-{tag}/{flag}")
+
+
+@pytest.mark.parametrize("name,cascade", [("serving_mix_bf16", False), ("serving_mix_bf16", True),
+                                          ("mixed", False), ("shared_prefix_decode_bf16", True)])
+def test_side_stream_fork_equals_serial_bitwise(name, cascade):
+    """A plan with tile and few-row work runs the few-row kernel on a side
+    stream; with MSTAR_FLAG_SERIAL everything runs on the caller's stream.  The
+    kernels do the same arithmetic either way: bitwise equal outputs."""
+    import torch
+
+    b = W.reduced(name)
+    t = W.make_tensors_torch(b, DEV)
+    pl = plan_for(b, 0, cascade=cascade)
+    st = pl.stats()
+    assert st["decode_items"] > 0 and (st["prefill_items"] > 0 or len(pl.items(4)) > 0)  # forks or not
+    pl.destroy()
+    o1, l1 = run_gpu(b, t, 0, cascade=cascade)
+    o2, l2 = run_gpu(b, t, attn.FLAG_SERIAL, cascade=cascade)
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1.view(torch.int32), l2.view(torch.int32))
+    _compare(b, o1, l1, *_oracle(b, t), f"{name} fork")
 
 
 @pytest.mark.parametrize("seed", [1, 2])
@@ -157,7 +178,8 @@ def test_fwd_rejects_wrong_shapes_and_small_workspace():
                                           ("text_latent_bf16", False), ("stream_window_bf16", False),
                                           ("rollout_bf16", False), ("cfg_labels_bf16", False),
                                           ("shared_prefix_decode_bf16", False), ("shared_prefix_decode_bf16", True),
-                                          ("rollout_bf16", True), ("cfg_labels_bf16", True)])
+                                          ("rollout_bf16", True), ("cfg_labels_bf16", True),
+                                          ("serving_mix_bf16", False), ("serving_mix_bf16", True)])
 def test_full_size_sampled(name, cascade):
     import torch
 

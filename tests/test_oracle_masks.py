@@ -155,3 +155,35 @@ def test_cfg_labels_full_size_counts_closed_form():
     assert w["pairs"] == 2 * 28 * 4096 * (8448 + 8192 + 4352)
     # distinct keys: per image 8448 + 8192 + 4096 (the text keys of the image-dropped label are shared)
     assert w["kv_bytes"] == 2 * 2 * (8448 + 8192 + 4096) * 4 * 128 * 2
+
+
+def test_serving_mix_each_request_kind_by_its_own_predicate():
+    """The node batch across Walks: decode rows see their whole context; the
+    image request's text rows are causal and blind to the latents, its latent
+    rows see everything; chunk rows are causal under a 96-key window; rollout
+    frames see the shared prefix and frames up to their own."""
+    b = W.reduced("serving_mix_bf16")
+    text, latent, Wn, prefix, frame = 37, 200, 96, 64, 40
+    kinds = ["decode"] * 5 + ["image"] + ["chunk"] * 4 + ["rollout"] * 3
+    assert len(kinds) == b.num_seqs
+    for r, kind in enumerate(kinds):
+        q_len, L = int(b.seqs[r, 0]), int(b.seqs[r, 1])
+        if kind == "decode":
+            pred = lambda p, t: t <= p  # noqa: E731
+            assert q_len == 1
+        elif kind == "image":
+            pred = lambda p, t: (t <= p) if p < text else True  # noqa: E731
+            assert q_len == L == text + latent
+        elif kind == "chunk":
+            pred = lambda p, t: t <= p and p - t < Wn  # noqa: E731
+            assert q_len == 16
+        else:
+            def pred(p, t):
+                return t < prefix or (t - prefix) // frame <= (p - prefix) // frame
+            assert q_len == 2 * frame and L == prefix + 2 * frame
+        assert np.array_equal(_vis(b, r), _brute(q_len, L, pred)), (r, kind)
+    first_roll = kinds.index("rollout")
+    shared = b.block_table[first_roll, :prefix // 16]
+    for r in range(first_roll, b.num_seqs):
+        assert np.array_equal(b.block_table[r, :prefix // 16], shared)
+    assert b.prefix_groups == [(list(range(first_roll, b.num_seqs)), prefix)]

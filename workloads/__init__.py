@@ -331,6 +331,54 @@ def mixed(seed: int = 0, hq: int = 8, hkv: int = 2, d: int = 128, dtype: str = "
     return b
 
 
+def serving_mix_bf16(seed: int = 0, n_decode: int = 48, lmin: int = 512, lmax: int = 8192, text: int = 256,
+                     latent: int = 4096, n_chunk: int = 64, cmin: int = 1024, cmax: int = 16384,
+                     window: int = 1024, n_roll: int = 16, prefix: int = 2048, frames: int = 2, frame: int = 256,
+                     hq: int = 28, hkv: int = 4, d: int = 128) -> Batch:
+    """One node's batch across Walks (Sec. 3.2: one LLM replica serves requests
+    at different graph positions in one launch): decode steps, one image
+    request's text + latent prefill, streaming speech chunks under a sliding
+    window, and world-model rollout frames over a shared context, with one
+    head layout.  The rollouts form a shared-prefix group."""
+    rng = _rng(seed, _SUB_LENGTHS)
+    q_lens, kv_lens, seg_lists, windows = [], [], [], []
+    for L in rng.integers(lmin, lmax + 1, size=n_decode):
+        L = int(L)
+        q_lens.append(1); kv_lens.append(L); seg_lists.append([(0, L, SEG_CAUSAL, 0)]); windows.append(0)
+    q_lens.append(text + latent); kv_lens.append(text + latent)
+    seg_lists.append([(0, text, SEG_CAUSAL, 0), (text, latent, SEG_FULL, 0)]); windows.append(0)
+    for C in rng.integers(cmin, cmax + 1, size=n_chunk):
+        C = int(C)
+        q_lens.append(16); kv_lens.append(C + 16); seg_lists.append([(0, C + 16, SEG_CAUSAL, 0)])
+        windows.append(window)
+    first_roll = len(kv_lens)
+    if prefix % PAGE:
+        raise ValueError("shared prefix must be page aligned")
+    for _ in range(n_roll):
+        q_lens.append(frames * frame); kv_lens.append(prefix + frames * frame)
+        seg_lists.append([(0, prefix, SEG_FULL, 0), (prefix, frames * frame, SEG_BLOCKS, frame)])
+        windows.append(0)
+    # private pages for every request; the rollouts' first prefix / 16 pages are shared
+    prng = _rng(seed, _SUB_PERM)
+    shared_pages = prefix // PAGE
+    need = [(x + PAGE - 1) // PAGE for x in kv_lens]
+    own = [need[r] - (shared_pages if r >= first_roll else 0) for r in range(len(need))]
+    pool = sum(own) + (shared_pages if n_roll else 0)
+    perm = prng.permutation(pool).astype(np.int32)
+    bt = np.full((len(kv_lens), max(need)), -1, dtype=np.int32)
+    cur = shared_pages if n_roll else 0
+    for r in range(len(kv_lens)):
+        off = 0
+        if r >= first_roll:
+            bt[r, :shared_pages] = perm[:shared_pages]
+            off = shared_pages
+        bt[r, off:off + own[r]] = perm[cur:cur + own[r]]
+        cur += own[r]
+    b = _finish("serving_mix_bf16", hq, hkv, d, "bf16", q_lens, kv_lens, seg_lists, windows, bt, pool, seed)
+    b.prefix_groups = [(list(range(first_roll, first_roll + n_roll)), prefix)] if n_roll else None
+    return b
+
+
 FULL_SIZE = {
     "tiny_causal_f32": tiny_causal_f32,
     "decode_bf16": decode_bf16,
@@ -339,6 +387,7 @@ FULL_SIZE = {
     "rollout_bf16": rollout_bf16,
     "cfg_labels_bf16": cfg_labels_bf16,
     "shared_prefix_decode_bf16": shared_prefix_decode_bf16,
+    "serving_mix_bf16": serving_mix_bf16,
 }
 
 
@@ -360,6 +409,9 @@ def reduced(name: str, seed: int = 0) -> Batch:
         return cfg_labels_bf16(seed, n=2, text=32, image=101, latent=70, hq=7, hkv=1)
     if name == "shared_prefix_decode_bf16":
         return shared_prefix_decode_bf16(seed, n=37, prefix=320, own_min=1, own_max=150, hq=8, hkv=2)
+    if name == "serving_mix_bf16":
+        return serving_mix_bf16(seed, n_decode=5, lmin=1, lmax=900, text=37, latent=200, n_chunk=4, cmin=1,
+                                cmax=600, window=96, n_roll=3, prefix=64, frames=2, frame=40, hq=7, hkv=1)
     if name == "mixed":
         return mixed(seed)
     raise KeyError(name)
