@@ -64,11 +64,6 @@ struct RowGroup {
     }
 };
 
-// Workgroup barrier for LDS hand-offs: waits for this wave's LDS (and scalar)
-// operations only, so global loads into registers stay in flight across it
-// (__syncthreads also waits for every outstanding global load).
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-
 __device__ __forceinline__ bf16x4 lds_read_tr16(const bf16_t* p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
 }
@@ -79,18 +74,6 @@ __device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
 
 __device__ __forceinline__ bf16x8 to_bf16x8(f32x4 a, f32x4 b) {
     return cat(__builtin_convertvector(a, bf16x4), __builtin_convertvector(b, bf16x4));
-}
-
-// Element offset of key t of KV head kvh, or -1 if its block-table entry is
-// outside the pool (recorded in the sticky error word; the key reads as 0).
-__device__ __forceinline__ int64_t kv_offset(const KArgs& a, const int32_t* bt_row, int32_t t,
-                                             int32_t kvh, int D) {
-    const int32_t page = bt_row[t >> 4];
-    if ((uint32_t)page >= (uint32_t)a.num_pages) {
-        atomicOr(a.err, 1);
-        return -1;
-    }
-    return (((int64_t)page * 16 + (t & 15)) * a.hkv + kvh) * D;
 }
 
 // K/V rows are read through a buffer resource per page: the page base lives in
@@ -244,28 +227,14 @@ __device__ __forceinline__ int v_swizzle(int row) {  // 16-byte chunk XOR for V 
     return D == 128 ? ((row & 7) << 1) : (((row >> 1) & 3) << 1);
 }
 
-// 16-byte direct global -> LDS load of one wave: lane i writes LDS bytes
-// [lds_addr + 16 i, +16).  Issued from assembly so that the compiler does not
-// put a wait for it in front of every LDS read (it cannot tell the tile being
-// read from the tile being filled); the kernel waits itself (dma_barrier)
-// before reading a filled tile.  (The few-row kernel, whose two buffers are
-// static, uses the compiler's builtin instead: lds_load16.)
-__device__ __forceinline__ void lds_dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
+// 4-byte direct global -> LDS load of one wave: lane i writes LDS bytes
+// [lds_addr + 4 i, +4).  Issued from assembly so that the compiler does not
+// track it (a tracked load in the tile loop makes the compiler wait for every
+// outstanding load before its result is first used); the kernel waits itself
+// (dma_barrier) before reading the filled bytes.
+__device__ __forceinline__ void lds_dma4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
     // M0 holds the (wave-uniform) LDS address; the compiler reserves M0, so
     // the asm puts its previous value back instead of declaring it clobbered
-    uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %3\n\t"
-        "buffer_load_dwordx4 %1, %2, 0 offen lds\n\t"
-        "s_mov_b32 m0, %0"
-        : "=&s"(saved)
-        : "v"(voff), "s"(r), "s"(__builtin_amdgcn_readfirstlane(lds_addr))
-        : "memory");
-}
-// 4-byte direct global -> LDS load of one wave: lane i writes LDS bytes
-// [lds_addr + 4 i, +4).  Untracked by the compiler, like lds_dma16.
-__device__ __forceinline__ void lds_dma4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds_addr) {
     uint32_t saved;
     asm volatile(
         "s_mov_b32 %0, m0\n\t"
@@ -732,10 +701,7 @@ __global__ __launch_bounds__(256, RB == 4 ? 1 : 2) void few_kernel(KArgs a) {
     int32_t pw_cur = load_pages(0), pw_next = my_steps > 32 ? load_pages(32) : 0;
     const int64_t slot_stride = (int64_t)a.hkv * D;
 
-    // Loads are issued unconditionally from in-pool addresses (a key past the
-    // item's end, or on a page outside the pool, reads some valid slot) and a
-    // per-lane mask marks the rows to zero at compute time: predicated loads
-    // would make the compiler wait for every outstanding load.
+    // K of one step, straight into MFMA operand registers
     struct Step {
         uint4 k[2][DS];
     };

@@ -13,13 +13,19 @@
 //     row sees every key up to the end of its own block, and a window only
 //     cuts keys off from below);
 //  3. cut the batch into work items: few-row items (decode-like requests whose
-//     query rows times grouped heads fit one 64-row item; all query heads of a
-//     KV head share one stream of K/V) and 128-row tiles of one query head for
-//     everything else;
+//     query rows times grouped heads fit one 64-row item, at most 32 rows per
+//     item at head_dim 128; all query heads of a KV head share one stream of
+//     K/V) and 128-row tiles of one query head for everything else; with
+//     shared-prefix groups (a cascade), the prefix of each group is cut into
+//     128-row items over the decode-like members' (row, head) list and the
+//     members' own items start at the prefix end;
 //  4. split key ranges into chunks when there are too few items to fill the
 //     GPU (partials are merged by their log-sum-exps afterwards);
 //  5. order every list longest first so that the hardware dispatcher, which
-//     starts workgroups in order as slots free up, ends with short items.
+//     starts workgroups in order as slots free up, ends with short items;
+//  6. lay out the multi-row workgroups (tiles, cascade items) so that the
+//     readers of one request's pages for one KV head share an XCD and its L2;
+//  7. the KV-append items: the step's new rows of each request, 16 per item.
 #include "planner.h"
 
 #include <algorithm>
