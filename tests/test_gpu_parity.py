@@ -122,6 +122,41 @@ def test_determinism_and_page_permutation_bitwise():
     assert torch.equal(l1.view(torch.int32), l3.view(torch.int32))
 
 
+@pytest.mark.parametrize("name,cascade", [("mixed", False), ("serving_mix_bf16", False), ("mixed", True),
+                                          ("decode_bf16", False)])
+def test_pool_beyond_2gb_takes_per_page_resources(name, cascade):
+    """A K/V pool larger than 2 GB takes the kernels' per-page buffer-resource
+    path (one resource per page instead of one per pool).  The batch's pages
+    are moved to the top of a pool of just over 2 GB (byte offsets past 2^31)
+    and the results must equal the compact batch's bitwise."""
+    import dataclasses
+
+    import torch
+
+    b = W.reduced(name)
+    t = W.make_tensors_torch(b, DEV)
+    o_ref, l_ref = run_gpu(b, t, attn.FLAG_FORCE_SPLIT, cascade=cascade)
+    page_bytes = 16 * b.num_kv_heads * b.head_dim * 2
+    big = (1 << 31) // page_bytes + b.num_pages + 64
+    assert (big - b.num_pages) * page_bytes > (1 << 31)
+    # page p -> big - 1 - p: every page sits past the 2 GB mark
+    bt = b.block_table.copy()
+    valid = bt >= 0
+    bt[valid] = big - 1 - bt[valid]
+    nb = dataclasses.replace(b, block_table=bt, num_pages=big)
+    nt = dict(t)
+    idx = torch.arange(big - 1, big - 1 - b.num_pages, -1, device=DEV)
+    for k in ("k_pages", "v_pages"):
+        x = torch.zeros((big,) + tuple(t[k].shape[1:]), dtype=t[k].dtype, device=DEV)
+        x[idx] = t[k]
+        nt[k] = x
+    o, l = run_gpu(nb, nt, attn.FLAG_FORCE_SPLIT, cascade=cascade)
+    assert torch.equal(o.view(torch.int16), o_ref.view(torch.int16))
+    assert torch.equal(l.view(torch.int32), l_ref.view(torch.int32))
+    del nt
+    torch.cuda.empty_cache()
+
+
 def test_unused_slots_poisoned_with_nan():
     for name in ("mixed", "decode_bf16", "rollout_bf16", "tiny_causal_f32"):
         b = W.reduced(name)
