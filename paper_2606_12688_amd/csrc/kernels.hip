@@ -264,9 +264,15 @@ __device__ __forceinline__ void wait_vmem() {
 // builtin (lane i writes bytes [16 i, 16 i + 16) after `lds`, which must be
 // wave-uniform).  The compiler tracks it: it waits for it before a read of
 // the same LDS array, so buffers that must not be waited for together live
-// in distinct arrays.
-__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, void* lds) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(lds), 16, voff, 0, 0, 0);
+// in distinct arrays.  The load is marked non-temporal (the NT cache-policy bit): the few-row
+// kernel reads each V row of a request once, so its lines go first when the
+// caches need room (decode batch: 0.617 -> 0.676 of HBM peak; 16-token
+// chunks: 0.593 -> 0.618).  Marking the K loads into registers as well was
+// slower on the chunk batch (0.571).
+constexpr int kCachePolicyNT = 2;
+__device__ __forceinline__ void lds_load16_nt(__amdgpu_buffer_rsrc_t r, uint32_t voff, void* lds) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(lds), 16, voff, 0, 0,
+                                             kCachePolicyNT);
 }
 // The same with a wave-uniform scalar byte offset added to the global address.
 __device__ __forceinline__ void lds_load16s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, void* lds) {
@@ -769,7 +775,7 @@ __global__ __launch_bounds__(256, RB == 4 ? 1 : 2) void few_kernel(KArgs a) {
             const int row = j * RPL + lane / CH;
             const int h = (j * RPL) >> 4;  // page half of the load's rows: the same across the wave
             const bool live = !tail || k0 + row < it.k_end;
-            lds_load16(rv[h], live ? voff[j % VJ] : kOutOfRange, &vs[wave_u][j * 1024]);
+            lds_load16_nt(rv[h], live ? voff[j % VJ] : kOutOfRange, &vs[wave_u][j * 1024]);
         }
     };
 
