@@ -184,15 +184,17 @@ def bench_serve(args, b, dev):
     out = torch.empty_like(t["q"])
     lse = torch.empty(t["q"].shape[:2], dtype=torch.float32, device=dev)
     bt = torch.from_numpy(np.ascontiguousarray(b.block_table)).to(dev)
+    flags = attn.FLAG_SERIAL if args.serial else 0
     args_plan = (b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, b.seqs, b.masks, b.segments,
-                 b.block_table.shape[1], b.num_pages, b.sm_scale, 0)
-    pl0 = attn.plan(*args_plan, stream)
+                 b.block_table.shape[1], b.num_pages, b.sm_scale, flags)
+    groups = b.prefix_groups if args.cascade else None
+    pl0 = attn.plan(*args_plan, stream, prefix_groups=groups)
     ws = attn.workspace(pl0, dev)  # the same shapes every step: one workspace
     pl0.destroy()
 
     def inline(n):
         for _ in range(n):
-            pl = attn.plan(*args_plan, stream)
+            pl = attn.plan(*args_plan, stream, prefix_groups=groups)
             attn.fwd(pl, t["q"], t["k_pages"], t["v_pages"], bt, out, lse, ws, stream)
             torch.cuda.synchronize()
             pl.destroy()
@@ -200,10 +202,10 @@ def bench_serve(args, b, dev):
     ap = attn.AsyncPlanner(depth=2)
 
     def overlapped(n):
-        ap.submit(*args_plan)
+        ap.submit(*args_plan, prefix_groups=groups)
         for i in range(n):
             if i + 1 < n:
-                ap.submit(*args_plan)
+                ap.submit(*args_plan, prefix_groups=groups)
             pl = ap.take(stream)
             attn.fwd(pl, t["q"], t["k_pages"], t["v_pages"], bt, out, lse, ws, stream)
             torch.cuda.synchronize()
@@ -216,14 +218,15 @@ def bench_serve(args, b, dev):
         fn(args.steps)
         res[name] = (time.perf_counter() - t0) * 1e3 / args.steps
     ap.close()
-    st = attn.plan(*args_plan[:-1], attn.FLAG_HOST_ONLY)
+    st = attn.plan(*args_plan[:-1], flags | attn.FLAG_HOST_ONLY, prefix_groups=groups)
     plan_us = st.stats()["plan_host_us"]
     st.destroy()
     print(json.dumps({
         "metric": "serving-loop step time, plan + attention + wait (ms)", "value": round(res["async"], 5),
         "unit": "ms", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(res["async"], 5),
         "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": b.dtype, "data": "synthetic",
-        "config": dict(describe(b), op="serve"), "inline_ms_per_step": round(res["inline"], 5),
+        "config": dict(describe(b), op="serve", cascade=bool(args.cascade)),
+        "inline_ms_per_step": round(res["inline"], 5),
         "async_ms_per_step": round(res["async"], 5), "plan_host_us": round(plan_us, 1)}), flush=True)
 
 
@@ -272,6 +275,9 @@ def main():
     from paper_2606_12688_amd import attn
 
     b = W.FULL_SIZE[args.workload](args.seed)
+    if args.cascade and not b.prefix_groups:
+        print(f"{args.workload} declares no shared-prefix group", file=sys.stderr)
+        sys.exit(2)
     if args.op == "append":
         bench_append(args, b, dev)
         return
@@ -280,9 +286,6 @@ def main():
         return
     bound = BOUND[args.workload]
     stream = torch.cuda.current_stream()
-    if args.cascade and not b.prefix_groups:
-        print(f"{args.workload} declares no shared-prefix group", file=sys.stderr)
-        sys.exit(2)
 
     def make_plan():
         return attn.plan(b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, b.seqs, b.masks, b.segments,
