@@ -41,6 +41,12 @@
 #ifndef MSTAR_FEW_TARGET_ITEMS
 #define MSTAR_FEW_TARGET_ITEMS 512
 #endif
+// Cascade items: the shared prefix is cut into chunks until the items reach
+// about this many workgroups.  Every chunk adds an fp32 partial per member row
+// to write and merge (shared-prefix decode: 256 beat 128, 512 and 1024).
+#ifndef MSTAR_CASCADE_TARGET_WGS
+#define MSTAR_CASCADE_TARGET_WGS 256
+#endif
 
 namespace mstar {
 namespace {
@@ -378,7 +384,8 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             const int64_t R = group_rows[g] * G;
             if (R == 0) continue;  // no member joined, or none has a query row
             int64_t nch = 1;
-            if (!(P.flags & MSTAR_FLAG_NO_SPLIT) && tiles > 0 && tiles < 512) nch = ceil_div(512, tiles);
+            if (!(P.flags & MSTAR_FLAG_NO_SPLIT) && tiles > 0 && tiles < MSTAR_CASCADE_TARGET_WGS)
+                nch = ceil_div(MSTAR_CASCADE_TARGET_WGS, tiles);
             if (P.flags & MSTAR_FLAG_FORCE_SPLIT) nch = 3;
             nch = std::max<int64_t>(1, std::min<int64_t>(nch, gr.prefix_len / (2 * kTileKeys)));
             const int64_t cs = ceil_div(ceil_div(gr.prefix_len, nch), kTileKeys) * kTileKeys;
