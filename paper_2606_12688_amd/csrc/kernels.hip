@@ -39,6 +39,14 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Workgroup and work-item indices straight from the hardware.  The runtime
+// library's blockIdx / threadIdx accessors are not inlined into functions built
+// with the IEEE mode bit off (their attributes differ), so they would be real
+// calls returning the indices in vector registers, and everything derived from
+// the workgroup index (item, bounds, loop counts) would leave scalar registers.
+__device__ __forceinline__ int wg_id() { return (int)__builtin_amdgcn_workgroup_id_x(); }
+__device__ __forceinline__ int thread_id() { return (int)__builtin_amdgcn_workitem_id_x(); }
+
 // Reductions over the four lanes l, l^16, l^32, l^48 that share a query row,
 // with gfx950's permlane swaps (v_permlane32_swap exchanges the upper half-wave
 // of one register with the lower half of another; with both operands the same
@@ -290,8 +298,11 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
 // valid offset in range and pushes the marker offset below out of range.
 constexpr uint32_t kSmallPoolBytes = 0x80000000u;
 
+// Occupancy: two workgroups per CU at d = 128 (64 KB of LDS and up to 256
+// VGPRs each), four at d = 64 (32 KB, at most 128 VGPRs: the softmax's vector
+// work, which bounds d = 64, then has four waves per SIMD to draw from).
 template <int D, int RBW, bool SMALL, bool CASC>
-__global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
+__global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
     constexpr int BN = kTileKeys;
     constexpr int RBY = 2 * D;       // bytes per K/V row in LDS
     constexpr int CH = D / 8;        // 16-byte chunks per row
@@ -311,14 +322,14 @@ __global__ __launch_bounds__(256, 2) void tile_kernel(KArgs a) {
     // The planner's launch order names the (item, query head) of every
     // workgroup; it keeps the workgroups that read the same K/V pages on one
     // XCD.  Padding entries (item < 0) exit.
-    const int item = a.order[2 * blockIdx.x], head = a.order[2 * blockIdx.x + 1];
+    const int item = a.order[2 * wg_id()], head = a.order[2 * wg_id() + 1];
     if (item < 0) return;
     const int kvh = head / a.group;
     const WorkItem it = a.items[item];
     const SeqInfo si = a.seqs[it.seq];
     // the wave index is wave-uniform; readfirstlane lets the compiler keep
     // everything derived from it (row bounds, loop decisions) in scalars
-    const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3, lane = tid & 63;
+    const int tid = thread_id(), wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3, lane = tid & 63;
     const int n = lane & 15, grp = lane >> 4;
     const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
     const RowGroup rg;
@@ -646,9 +657,9 @@ __global__ __launch_bounds__(256, RB == 4 ? 1 : 2) void few_kernel(KArgs a) {
     __shared__ float ml_lds[4][2][RB * 16];
     __shared__ float fin_lds[2][RB * 16];
 
-    const WorkItem it = a.items[blockIdx.x];
+    const WorkItem it = a.items[wg_id()];
     const SeqInfo si = a.seqs[it.seq];
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int tid = thread_id(), wave = tid >> 6, lane = tid & 63;
     const int n = lane & 15, grp = lane >> 4;
     const int G = a.group;
     const int kvh = it.head;
@@ -942,9 +953,9 @@ template <int D>
 __global__ __launch_bounds__(256) void f32_kernel(KArgs a) {
     constexpr int E = D / 64;
     __shared__ float q_lds[4][D];
-    const WorkItem it = a.items[blockIdx.x];
+    const WorkItem it = a.items[wg_id()];
     const SeqInfo si = a.seqs[it.seq];
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wave = thread_id() >> 6, lane = thread_id() & 63;
     const int r = wave;
     if (r >= it.nrows) return;
     const int i = it.row0 + r;
@@ -1022,8 +1033,8 @@ __global__ __launch_bounds__(256) void f32_kernel(KArgs a) {
 template <int D, bool BF16>
 __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
     constexpr int E = D / 64;
-    const int idx = blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
+    const int idx = wg_id() * 4 + (thread_id() >> 6);
+    const int lane = thread_id() & 63;
     if (idx >= a.n_items) return;
     const MergeItem mi = a.items[idx];
     // slot set 1: slot0 + s * stride, s < nslots (split key ranges of the row's
@@ -1098,9 +1109,9 @@ __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
 // skipped and sets the error word.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void append_kernel(AArgs a) {
-    const WorkItem it = a.items[blockIdx.x];
+    const WorkItem it = a.items[wg_id()];
     const SeqInfo si = a.seqs[it.seq];
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & 3, lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(thread_id() >> 6) & 3, lane = thread_id() & 63;
     const int chunks = a.row_bytes >> 4;
     const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
     bool bad = false;
