@@ -394,3 +394,19 @@ def test_few_row_items_hold_at_most_32_rows_at_d128(d, limit):
     rows = [int(x[3]) for x in pl.items(1)]
     assert rows and max(rows) == limit
     pl.destroy()
+
+
+def test_near_equal_units_that_fill_the_gpu_stay_whole():
+    """Decode units that already number at least one per workgroup slot and
+    differ by less than a quarter of a piece are not split (no merge launch);
+    one much longer unit among them brings the splitting back."""
+    b = W.decode_bf16(seed=5, n=128, lmin=4096, lmax=4600, hq=28, hkv=4, pool_pages=None)
+    pl = plan_for(b, attn.FLAG_HOST_ONLY)
+    st = pl.stats()
+    assert st["decode_items"] == 128 * 4 and st["merge_rows"] == 0
+    assert all(int(x[6]) < 0 for x in pl.items(1))
+    pl.destroy()
+    b = W.decode_bf16(seed=5, n=128, lmin=4096, lmax=16384, hq=28, hkv=4, pool_pages=None)
+    pl = plan_for(b, attn.FLAG_HOST_ONLY)
+    assert pl.stats()["merge_rows"] > 0
+    pl.destroy()
