@@ -251,10 +251,12 @@ def test_full_size_sampled(name, cascade):
 
 
 @pytest.mark.parametrize("flag", ["auto", "force_split"])
-@pytest.mark.parametrize("name,rate", [("decode_bf16", 0.03), ("text_latent_bf16", 0.03),
-                                       ("stream_window_bf16", 0.03), ("rollout_bf16", 0.05),
-                                       ("decode_bf16", -0.0006)])
-def test_growing_scores_move_the_lazy_reference(name, rate, flag):
+@pytest.mark.parametrize("name,rate,cascade", [("decode_bf16", 0.03, False), ("text_latent_bf16", 0.03, False),
+                                               ("stream_window_bf16", 0.03, False), ("rollout_bf16", 0.05, False),
+                                               ("decode_bf16", -0.0006, False),
+                                               ("shared_prefix_decode_bf16", 0.03, True),
+                                               ("rollout_bf16", 0.05, True)])
+def test_growing_scores_move_the_lazy_reference(name, rate, cascade, flag):
     """Keys scaled by 1 + rate * position: with rate > 0 a row's maximum keeps
     growing from tile to tile, by about the lazy threshold of 2^8 per 64-key
     tile, so the kernels both keep a stale reference (probabilities up to 2^8)
@@ -278,6 +280,7 @@ def test_growing_scores_move_the_lazy_reference(name, rate, flag):
                 scale[p] = 1.0 + rate * (16 * j + np.arange(16))
     s = torch.from_numpy(scale).to(DEV)[:, :, None, None]
     t["k_pages"] = (t["k_pages"].float() * s).to(t["k_pages"].dtype)
-    out, lse = run_gpu(b, t, FLAGS[flag])
+    extra = attn.FLAG_CASCADE_ALL if cascade else 0
+    out, lse = run_gpu(b, t, FLAGS[flag] | extra, cascade=cascade)
     ro, rl = _oracle(b, t)
-    _compare(b, out, lse, ro, rl, f"{name}/rate {rate}/{flag}", rel_o=2.0**-8)
+    _compare(b, out, lse, ro, rl, f"{name}/rate {rate}/cascade {cascade}/{flag}", rel_o=2.0**-8)
