@@ -1044,11 +1044,22 @@ __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
         return s < mi.nslots ? mi.slot0 + (int64_t)s * mi.stride : mi.pad0 + (int64_t)(s - mi.nslots) * mi.pad1;
     };
     const int n = mi.nslots + mi.pad2;
+    // The rows of the first four slots are requested together with the LSEs
+    // (their addresses need only the item), so a row with few slots waits for
+    // one round trip to memory instead of three.
+    float v0[4][E];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int64_t slot = slot_of(u < n ? u : 0);
+#pragma unroll
+        for (int e = 0; e < E; ++e) v0[u][e] = u < n ? a.part_o[slot * D + lane + 64 * e] : 0.0f;
+    }
     // the slots' LSEs are read across the lanes, 64 at a time, and reduced
     // over the wave (a fixed order: the result does not depend on timing)
-    float mstar = kNegInf;
+    float mstar = kNegInf, x0 = kNegInf;
     for (int s0 = 0; s0 < n; s0 += 64) {
         float x = s0 + lane < n ? a.part_lse[slot_of(s0 + lane)] : kNegInf;
+        if (s0 == 0) x0 = x;
         for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
         mstar = fmaxf(mstar, x);
     }
@@ -1058,13 +1069,25 @@ __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
     if (mstar != kNegInf) {
         for (int s0 = 0; s0 < n; s0 += 64) {
             const int cnt = min(64, n - s0);
-            // lane j holds the weight of slot s0 + j
-            float w = lane < cnt ? expf(a.part_lse[slot_of(s0 + lane)] - mstar) : 0.0f;
+            // lane j holds the weight of slot s0 + j (the first 64 LSEs are
+            // still in registers)
+            const float xl = s0 == 0 ? x0 : (lane < cnt ? a.part_lse[slot_of(s0 + lane)] : kNegInf);
+            float w = lane < cnt ? expf(xl - mstar) : 0.0f;
             float ws = w;
             for (int off = 32; off > 0; off >>= 1) ws += __shfl_xor(ws, off, 64);
             tot += ws;
-            // four slots' rows loaded together, then accumulated in slot order
+            // slots in order; four rows loaded together
             int j = 0;
+            if (s0 == 0) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const float wj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), u));
+#pragma unroll
+                    for (int e = 0; e < E; ++e)
+                        if (u < cnt) acc[e] = fmaf(wj, v0[u][e], acc[e]);
+                }
+                j = 4;
+            }
             for (; j + 4 <= cnt; j += 4) {
                 float v[4][E];
 #pragma unroll
