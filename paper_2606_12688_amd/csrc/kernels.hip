@@ -659,7 +659,7 @@ __global__ __launch_bounds__(256, RB == 4 ? 1 : 2) void few_kernel(KArgs a) {
 
     const WorkItem it = a.items[wg_id()];
     const SeqInfo si = a.seqs[it.seq];
-    const int tid = thread_id(), wave = tid >> 6, lane = tid & 63;
+    const int tid = thread_id(), wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3, lane = tid & 63;
     const int n = lane & 15, grp = lane >> 4;
     const int G = a.group;
     const int kvh = it.head;
