@@ -1033,7 +1033,9 @@ __global__ __launch_bounds__(256) void f32_kernel(KArgs a) {
 template <int D, bool BF16>
 __global__ __launch_bounds__(256) void merge_kernel(MArgs a) {
     constexpr int E = D / 64;
-    const int idx = wg_id() * 4 + (thread_id() >> 6);
+    // one row per wave; the wave index is made scalar so that the item is
+    // read with scalar loads
+    const int idx = wg_id() * 4 + (__builtin_amdgcn_readfirstlane(thread_id() >> 6) & 3);
     const int lane = thread_id() & 63;
     if (idx >= a.n_items) return;
     const MergeItem mi = a.items[idx];
