@@ -79,38 +79,49 @@ def describe(b) -> dict:
 
 
 def cpu_baseline(b, tensors, unit, budget_s=15.0):
-    """The oracle, as it stands, on a sample of the workload's requests sized to
-    take about ``budget_s`` seconds of host time; scaled to the metric's unit."""
+    """The oracle, as it stands, timed on this host on a bounded sample of the
+    workload (about ``budget_s`` seconds of wall time), scaled to the metric's
+    unit.  The sample is whole requests (every query head) when one request
+    fits the budget several times over, else the first query heads of one
+    request (a full-size text+latent request alone takes tens of seconds)."""
     import workloads as W
     from oracle import oracle_attention
     from paper_2606_12688_amd import attn
 
-    def measure(reqs):
+    def measure(reqs, heads):
         sb, q, kp, vp, _ = W.extract_requests(b, tensors, reqs)
         pl = attn.plan(sb.num_qo_heads, sb.num_kv_heads, sb.head_dim, sb.dtype, sb.seqs, sb.masks,
                        sb.segments, sb.block_table.shape[1], sb.num_pages, sb.sm_scale, attn.FLAG_HOST_ONLY)
         pairs, kr = pl.stats()["visible_pairs"], pl.key_ranges()
         pl.destroy()
+        frac = len(heads) / b.num_qo_heads
+        kv_heads = len({h // (b.num_qo_heads // b.num_kv_heads) for h in heads})
         c0, t0 = time.process_time(), time.perf_counter()
-        oracle_attention(sb, q, kp, vp)
+        oracle_attention(sb, q, kp, vp, heads=heads)
         wall = time.perf_counter() - t0
-        return wall, time.process_time() - c0, pairs, kv_bytes(sb, kr)
+        return wall, time.process_time() - c0, pairs * frac, kv_bytes(sb, kr) * kv_heads / b.num_kv_heads
 
     order = np.random.default_rng(123).permutation(b.num_seqs)
-    wall1, _, _, _ = measure(order[:1])
-    n = int(max(1, min(b.num_seqs, budget_s / max(wall1, 1e-3))))
-    wall, cpu, pairs, nbytes = measure(order[:n])
+    all_heads = list(range(b.num_qo_heads))
+    w1, _, _, _ = measure(order[:1], [0])  # one request, one head
+    if w1 * b.num_qo_heads * 3 <= budget_s:
+        heads = all_heads
+        n = int(max(1, min(b.num_seqs, budget_s / max(w1 * b.num_qo_heads, 1e-3))))
+    else:
+        n = 1
+        heads = all_heads[:int(max(1, min(b.num_qo_heads, budget_s / max(w1, 1e-3))))]
+    wall, cpu, pairs, nbytes = measure(order[:n], heads)
     reps = 1
-    while wall < budget_s * 0.66 and reps < 100:  # a small workload: repeat it (wall, cpu are totals)
-        w2, c2, _, _ = measure(order[:n])
+    while wall < budget_s * 0.66 and reps < 100:  # a small sample: repeat it (wall, cpu are totals)
+        w2, c2, _, _ = measure(order[:n], heads)
         wall, cpu, reps = wall + w2, cpu + c2, reps + 1
     wall, cpu = wall / reps, cpu / reps
     flop = 4.0 * b.head_dim * pairs
     value = nbytes / wall / 1e9 if unit == "GB/s" else flop / wall / 1e12
     return {"value": value, "unit": unit, "cores": max(1, int(round(cpu / wall))), "kind": "oracle",
-            "sample": f"{n} of {b.num_seqs} requests (all heads), fp64 NumPy oracle, mean of {reps} run(s) of {wall:.2f} s wall, "
-                      f"{flop / wall / 1e9:.2f} GFLOP/s, {nbytes / wall / 1e9:.3f} GB/s KV",
-            "host_threads_available": len(os.sched_getaffinity(0))}
+            "sample": f"{n} of {b.num_seqs} requests x {len(heads)} of {b.num_qo_heads} query heads, fp64 NumPy "
+                      f"oracle, mean of {reps} run(s) of {wall:.2f} s wall, {flop / wall / 1e9:.2f} GFLOP/s, "
+                      f"{nbytes / wall / 1e9:.3f} GB/s KV"}
 
 
 def bench_append(args, b, dev):
@@ -230,19 +241,199 @@ def bench_serve(args, b, dev):
         "async_ms_per_step": round(res["async"], 5), "plan_host_us": round(plan_us, 1)}), flush=True)
 
 
+CONFIGS = ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16", "rollout_bf16"]
+HEADLINE = "rollout_bf16"  # the largest configuration (3.38 TFLOP, 2.54 GB per step)
+
+
+def host_cpu():
+    """CPU model and the logical CPUs this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0))
+
+
+def bench_attention(args, name, dev, cpu_budget_s):
+    """One workload: build the plan, rotate input copies, time K steps of
+    ``mstar_attn_fwd`` with nothing else on the stream (the step time), then a
+    separate sampled loop with HIP events around each kernel (per-kernel
+    durations for the roofline).  Returns the per-configuration record."""
+    import torch
+
+    import workloads as W
+    from paper_2606_12688_amd import attn
+
+    b = W.FULL_SIZE[name](args.seed)
+    if args.cascade and not b.prefix_groups:
+        raise SystemExit(f"{name} declares no shared-prefix group")
+    bound = BOUND[name]
+    stream = torch.cuda.current_stream()
+
+    def make_plan():
+        return attn.plan(b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, b.seqs, b.masks, b.segments,
+                         b.block_table.shape[1], b.num_pages, b.sm_scale, attn.FLAG_SERIAL if args.serial else 0,
+                         stream, prefix_groups=b.prefix_groups if args.cascade else None)
+    # the first plan of a process includes one-time set-up (pools, HIP context
+    # work); the reported planning time is that of a later plan
+    pl_first = make_plan()
+    plan_first_us = pl_first.stats()["plan_host_us"]
+    pl_first.destroy()
+    plan_us = []
+    for _ in range(5):
+        p2 = make_plan()
+        plan_us.append(p2.stats()["plan_host_us"])
+        p2.destroy()
+    pl = make_plan()
+    st = pl.stats()
+    flop = 4.0 * b.head_dim * st["visible_pairs"]
+    nbytes = kv_bytes(b, pl.key_ranges())
+
+    # rotate enough copies that one step's K/V is out of the 256 MB MALL by the next use
+    n_rot = min(8, max(2, int(np.ceil(1.0e9 / max(nbytes, 1)))))
+    copies = []
+    for i in range(n_rot):
+        t = W.make_tensors_torch(b, dev, seed=args.seed + 1000 * i)
+        t["out"] = torch.empty_like(t["q"])
+        t["lse"] = torch.empty(t["q"].shape[:2], dtype=torch.float32, device=dev)
+        copies.append(t)
+    bt = torch.from_numpy(np.ascontiguousarray(b.block_table)).to(dev)
+    ws = attn.workspace(pl, dev)
+    # validate every copy once through the checked binding, then call the C entry point directly
+    for t in copies:
+        attn.fwd(pl, t["q"], t["k_pages"], t["v_pages"], bt, t["out"], t["lse"], ws, stream)
+    assert attn.check(pl, stream) == 0
+    L = attn.lib()
+    sh = stream.cuda_stream
+    ws_ptr, ws_n = (ws.data_ptr(), ws.numel()) if ws is not None else (None, 0)
+    calls = [(pl.handle, t["q"].data_ptr(), t["k_pages"].data_ptr(), t["v_pages"].data_ptr(), bt.data_ptr(),
+              t["out"].data_ptr(), t["lse"].data_ptr(), ws_ptr, ws_n, sh) for t in copies]
+
+    def run(i):
+        rc = L.mstar_attn_fwd(*calls[i % n_rot])
+        if rc != 0:
+            raise attn.MStarError(rc, attn.last_error())
+
+    # ---- the step time: K calls back to back, nothing else on the stream
+    K = args.steps
+    for i in range(args.warmup):
+        run(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        run(i)
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / K
+
+    # ---- per-kernel durations: a separate loop with the library's HIP events
+    # recorded right before / after each kernel on the stream it runs on, and
+    # a pair around the whole call on the caller's stream
+    launched = [k for k, n in enumerate(("prefill_items", "decode_items", "f32_items", "merge_rows")) if st[n] > 0]
+    if len(pl.items(4)):
+        launched.append(4)
+    n_ev = max(8, min(32, K))
+    evs = [[[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(2)] for _ in range(n_ev)]
+    span = [[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in range(n_ev)]
+    arrays = []
+    for i in range(n_ev):
+        arr = [(ctypes.c_void_p * 5)(), (ctypes.c_void_p * 5)()]
+        for side in range(2):
+            for k in launched:
+                evs[i][side][k].record(stream)  # creates the event
+                arr[side][k] = evs[i][side][k].cuda_event
+        arrays.append(arr)
+    torch.cuda.synchronize()
+    for i in range(n_ev):
+        span[i][0].record(stream)
+        rc = L.mstar_attn_fwd_timed(*calls[i % n_rot], arrays[i][0], arrays[i][1])
+        span[i][1].record(stream)
+        if rc != 0:
+            raise attn.MStarError(rc, attn.last_error())
+    torch.cuda.synchronize()
+    per_kernel = {KERNEL_NAMES[k]: np.array([evs[i][0][k].elapsed_time(evs[i][1][k]) for i in range(n_ev)])
+                  for k in launched}
+    span_ms = np.array([span[i][0].elapsed_time(span[i][1]) for i in range(n_ev)])
+    if len([k for k in launched if k in (0, 1, 4)]) > 1:
+        # the step's work is spread over several kernels, some side by side: the call's span
+        kernel_ms, dominant = span_ms, "call(" + "+".join(KERNEL_NAMES[k] for k in launched) + ")"
+    else:
+        dominant = KERNEL_NAMES[DOMINANT[name]]
+        kernel_ms = per_kernel[dominant]
+    assert attn.check(pl, stream) == 0
+
+    tflops = flop / (ms_per_step * 1e-3) / 1e12
+    gbps = nbytes / (ms_per_step * 1e-3) / 1e9
+    k_mean = float(kernel_ms.mean())
+    if bound == "hbm":
+        value, unit = gbps, "GB/s"
+        achieved, peak, runit = nbytes / (k_mean * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
+    elif bound == "mfma":
+        value, unit = tflops, "TFLOP/s"
+        achieved, peak, runit = flop / (k_mean * 1e-3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
+    else:
+        value, unit = tflops, "TFLOP/s"
+        achieved, peak, runit = flop / (k_mean * 1e-3) / 1e12, PEAK_FP32_TFLOPS, "TFLOP/s"
+
+    traffic = None
+    traffic_note = "no counter run recorded for this kernel source"
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f).get(name + ("+cascade" if args.cascade else ""))
+        if rec and rec.get("kernel_src_sha") == kernel_source_sha():
+            traffic = rec["hbm_bytes_per_launch"]
+            traffic_note = rec.get("note", "")
+        elif rec:
+            traffic_note = "kernels changed since the counters were taken"
+
+    def stats(v):
+        return {"mean": round(float(v.mean()), 5), "median": round(float(np.median(v)), 5),
+                "p95": round(float(np.percentile(v, 95)), 5)}
+
+    res = {
+        "workload": name, "value": round(value, 3), "unit": unit, "ms_per_step": round(ms_per_step, 5),
+        "dtype": b.dtype, "config": describe(b),
+        "roofline": {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": runit,
+                     "frac": round(achieved / peak, 4), "traffic": traffic},
+        "tflops": round(tflops, 3), "kv_gbps": round(gbps, 3),
+        "tflops_frac_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "kv_gbps_frac_hbm_peak": round(gbps / PEAK_HBM_GBS, 4),
+        "dominant_kernel": dominant, "kernel_ms": {k: stats(v) for k, v in per_kernel.items()},
+        "call_ms": stats(span_ms), "event_sampled_calls": n_ev,
+        "useful_flop": flop, "kv_bytes": nbytes, "plan_host_us": round(float(np.median(plan_us)), 1),
+        "plan_host_us_first_call": round(plan_first_us, 1),
+        "plan": {k: st[k] for k in ("prefill_items", "decode_items", "f32_items", "merge_rows", "partial_slots")},
+        "rotated_input_copies": n_rot, "traffic_note": traffic_note,
+    }
+    if cpu_budget_s > 0:
+        res["cpu_baseline"] = cpu_baseline(b, copies[0], unit, cpu_budget_s)
+    pl.destroy()
+    del copies, ws
+    torch.cuda.empty_cache()
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="decode_bf16", choices=sorted(BOUND))
+    ap.add_argument("--workload", default=None, choices=sorted(BOUND),
+                    help="time this workload only (default: the five configurations, rollouts as the headline)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle time for the headline's cpu_baseline (a third of it for each other "
+                         "configuration)")
     ap.add_argument("--serial", action="store_true",
                     help="plan with MSTAR_FLAG_SERIAL: every kernel on the caller's stream, none beside another")
     ap.add_argument("--cascade", action="store_true",
                     help="plan with the workload's shared-prefix groups (mstar_attn_plan_cascade); the roofline "
-                         "then divides by the summed time of every kernel of the step")
+                         "then divides by the span of the whole call")
     ap.add_argument("--op", default="attention", choices=["attention", "append", "serve"],
                     help="append: time mstar_kv_append (the step's new K/V rows into their pages); serve: a "
                          "serving loop that re-plans every step, planning inline vs on the async planner")
@@ -272,156 +463,44 @@ def main():
         return
 
     import workloads as W
-    from paper_2606_12688_amd import attn
 
-    b = W.FULL_SIZE[args.workload](args.seed)
-    if args.cascade and not b.prefix_groups:
-        print(f"{args.workload} declares no shared-prefix group", file=sys.stderr)
-        sys.exit(2)
-    if args.op == "append":
-        bench_append(args, b, dev)
+    if args.op in ("append", "serve"):
+        b = W.FULL_SIZE[args.workload or "decode_bf16"](args.seed)
+        if args.cascade and not b.prefix_groups:
+            print(f"{b.name} declares no shared-prefix group", file=sys.stderr)
+            sys.exit(2)
+        (bench_append if args.op == "append" else bench_serve)(args, b, dev)
         return
-    if args.op == "serve":
-        bench_serve(args, b, dev)
-        return
-    bound = BOUND[args.workload]
-    stream = torch.cuda.current_stream()
 
-    def make_plan():
-        return attn.plan(b.num_qo_heads, b.num_kv_heads, b.head_dim, b.dtype, b.seqs, b.masks, b.segments,
-                         b.block_table.shape[1], b.num_pages, b.sm_scale, attn.FLAG_SERIAL if args.serial else 0,
-                         stream, prefix_groups=b.prefix_groups if args.cascade else None)
-    # the first plan of a process includes one-time set-up (pinned staging, HIP
-    # context work); the reported planning time is that of a second plan
-    pl_first = make_plan()
-    plan_first_us = pl_first.stats()["plan_host_us"]
-    pl_first.destroy()
-    pl = make_plan()
-    st = pl.stats()
-    flop = 4.0 * b.head_dim * st["visible_pairs"]
-    nbytes = kv_bytes(b, pl.key_ranges())
-
-    # rotate enough copies that one step's K/V is out of the 256 MB MALL by the next use
-    n_rot = max(2, int(np.ceil(1.0e9 / max(nbytes, 1))))
-    n_rot = min(n_rot, 8)
-    copies = []
-    for i in range(n_rot):
-        t = W.make_tensors_torch(b, dev, seed=args.seed + 1000 * i)
-        t["out"] = torch.empty_like(t["q"])
-        t["lse"] = torch.empty(t["q"].shape[:2], dtype=torch.float32, device=dev)
-        copies.append(t)
-    bt = torch.from_numpy(np.ascontiguousarray(b.block_table)).to(dev)
-    ws = attn.workspace(pl, dev)
-    # validate every copy once through the checked binding, then call the C entry point directly
-    for t in copies:
-        attn.fwd(pl, t["q"], t["k_pages"], t["v_pages"], bt, t["out"], t["lse"], ws, stream)
-    assert attn.check(pl, stream) == 0
-    L = attn.lib()
-    sh = stream.cuda_stream
-    ws_ptr, ws_n = (ws.data_ptr(), ws.numel()) if ws is not None else (None, 0)
-    calls = [(pl.handle, t["q"].data_ptr(), t["k_pages"].data_ptr(), t["v_pages"].data_ptr(), bt.data_ptr(),
-              t["out"].data_ptr(), t["lse"].data_ptr(), ws_ptr, ws_n, sh) for t in copies]
-
-    # HIP events recorded by the library right before / after each kernel (on
-    # the stream the kernels run on) in about 16 evenly spaced steps of the
-    # timed region: each event pair costs a few microseconds of stream time,
-    # which would otherwise be charged to every step of a ~100 us workload
-    K = args.steps
-    launched = [k for k, n in enumerate(("prefill_items", "decode_items", "f32_items", "merge_rows")) if st[n] > 0]
-    if len(pl.items(4)):
-        launched.append(4)
-    stride = max(1, K // 16)
-    sampled = list(range(0, K, stride))
-    evs = {i: [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(2)] for i in sampled}
-    ev_arrays = {}
-    for i in sampled:
-        arr = [(ctypes.c_void_p * 5)(), (ctypes.c_void_p * 5)()]
-        for side in range(2):
-            for k in launched:
-                evs[i][side][k].record(stream)  # creates the event
-                arr[side][k] = evs[i][side][k].cuda_event
-        ev_arrays[i] = arr
-
-    # the whole call on the caller's stream (all kernels, forks and joins included)
-    span = {i: [torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for i in sampled}
-
-    def step(i, timed=False):
-        if timed and i in ev_arrays:
-            span[i][0].record(stream)
-            rc = L.mstar_attn_fwd_timed(*calls[i % n_rot], ev_arrays[i][0], ev_arrays[i][1])
-            span[i][1].record(stream)
-        else:
-            rc = L.mstar_attn_fwd(*calls[i % n_rot])
-        if rc != 0:
-            raise attn.MStarError(rc, attn.last_error())
-
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(K):
-        step(i, timed=True)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / K
-    per_kernel = {KERNEL_NAMES[k]: np.array([evs[i][0][k].elapsed_time(evs[i][1][k]) for i in sampled])
-                  for k in launched}
-    span_ms = np.array([span[i][0].elapsed_time(span[i][1]) for i in sampled])
-    if len([k for k in launched if k in (0, 1, 4)]) > 1:
-        # the step's work is spread over several kernels, some side by side: the call's span
-        kernel_ms = span_ms
-        dominant = "call(" + "+".join(KERNEL_NAMES[k] for k in launched) + ")"
+    budget = 0.0 if args.no_cpu_baseline else args.cpu_budget
+    model, nproc = host_cpu()
+    if args.workload:
+        names, head = [args.workload], args.workload
     else:
-        kernel_ms = per_kernel[KERNEL_NAMES[DOMINANT[args.workload]]]
-        dominant = KERNEL_NAMES[DOMINANT[args.workload]]
-    assert attn.check(pl, stream) == 0
-
-    tflops = flop / (ms_per_step * 1e-3) / 1e12
-    gbps = nbytes / (ms_per_step * 1e-3) / 1e9
-    k_mean = float(kernel_ms.mean())
-    if bound == "hbm":
-        value, unit = gbps, "GB/s"
-        achieved, peak, runit = nbytes / (k_mean * 1e-3) / 1e9, PEAK_HBM_GBS, "GB/s"
-    elif bound == "mfma":
-        value, unit = tflops, "TFLOP/s"
-        achieved, peak, runit = flop / (k_mean * 1e-3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
-    else:
-        value, unit = tflops, "TFLOP/s"
-        achieved, peak, runit = flop / (k_mean * 1e-3) / 1e12, PEAK_FP32_TFLOPS, "TFLOP/s"
-
-    traffic = None
-    traffic_note = "no counter run recorded for this kernel source"
-    if os.path.exists(TRAFFIC_FILE):
-        with open(TRAFFIC_FILE) as f:
-            rec = json.load(f).get(args.workload + ("+cascade" if args.cascade else ""))
-        if rec and rec.get("kernel_src_sha") == kernel_source_sha():
-            traffic = rec["hbm_bytes_per_launch"]
-            traffic_note = rec.get("note", "")
-        elif rec:
-            traffic_note = "kernels changed since the counters were taken"
-
+        names, head = CONFIGS, HEADLINE
+    configs = {}
+    for name in names:
+        print(f"[bench] {name}", file=sys.stderr, flush=True)
+        configs[name] = bench_attention(args, name, dev, budget if name == head else budget / 3)
+        if "cpu_baseline" in configs[name]:
+            configs[name]["cpu_baseline"].update(cpu_model=model, host_logical_cpus=nproc)
+    h = configs[head]
     res = {
-        "metric": METRIC, "value": round(value, 3), "unit": unit, "n_gpus": 1, "steps": K, "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": b.dtype, "data": "synthetic", "config": describe(b),
-        "roofline": {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": runit,
-                     "frac": round(achieved / peak, 4), "traffic": traffic},
-        "tflops": round(tflops, 3), "kv_gbps": round(gbps, 3),
-        "tflops_frac_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4), "kv_gbps_frac_hbm_peak": round(gbps / PEAK_HBM_GBS, 4),
-        "dominant_kernel": dominant, "cascade": bool(args.cascade), "serial": bool(args.serial),
-        "kernel_ms": {name: {"mean": round(float(v.mean()), 5), "median": round(float(np.median(v)), 5),
-                             "p95": round(float(np.percentile(v, 95)), 5)} for name, v in per_kernel.items()},
-        "call_ms": {"mean": round(float(span_ms.mean()), 5), "median": round(float(np.median(span_ms)), 5),
-                    "p95": round(float(np.percentile(span_ms, 95)), 5)},
-        "useful_flop": flop, "kv_bytes": nbytes, "plan_host_us": round(st["plan_host_us"], 1),
-        "plan_host_us_first_call": round(plan_first_us, 1), "event_sampled_steps": len(sampled),
-        "plan": {k: st[k] for k in ("prefill_items", "decode_items", "f32_items", "merge_rows", "partial_slots")},
-        "rotated_input_copies": n_rot, "traffic_note": traffic_note,
+        "metric": METRIC, "value": h["value"], "unit": h["unit"], "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": h["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": h["dtype"], "data": "synthetic",
+        "config": h["config"], "roofline": h["roofline"],
     }
-    if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(b, copies[0], unit)
+    if "cpu_baseline" in h:
+        res["cpu_baseline"] = h["cpu_baseline"]
+    res.update({k: v for k, v in h.items() if k not in res and k not in ("workload",)})
+    res["cascade"], res["serial"] = bool(args.cascade), bool(args.serial)
+    if len(names) > 1:
+        res["configs"] = {f"c{CONFIGS.index(n) + 1}_{n}": {
+            k: configs[n][k] for k in ("value", "unit", "ms_per_step", "roofline", "cpu_baseline", "tflops",
+                                       "kv_gbps", "useful_flop", "kv_bytes", "dominant_kernel", "kernel_ms",
+                                       "call_ms", "plan_host_us", "config") if k in configs[n]} for n in names}
     print(json.dumps(res), flush=True)
-    pl.destroy()
 
 
 if __name__ == "__main__":

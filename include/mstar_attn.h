@@ -39,6 +39,7 @@
 #ifndef MSTAR_ATTN_H
 #define MSTAR_ATTN_H
 
+#include <hip/hip_runtime_api.h> /* hipStream_t, hipEvent_t */
 #include <stddef.h>
 #include <stdint.h>
 
@@ -153,17 +154,23 @@ typedef struct {
  * spans, few-row items for decode-like requests, key ranges split into chunks
  * when there are too few items to fill the GPU), orders them longest first,
  * and uploads the work list with an async host-to-device copy enqueued on
- * `upload_stream` (a hipStream_t; NULL = default stream).  The caller must
- * order that upload before fwd (same stream, or synchronize).  Allocates
- * device memory for the work list (owned by the plan).  On success *out is a
- * new plan; on failure *out is NULL.
+ * `upload_stream` (NULL = default stream).  The caller must order that upload
+ * before fwd (same stream, or synchronize).  The work list's device buffer,
+ * its pinned staging copy and (for a plan whose fwd runs the few-row kernel
+ * beside the tile kernel) a side stream come from a per-device pool that
+ * destroyed plans return them to: only the first plans of a process, or a
+ * plan larger than every pooled buffer, allocate (hipMalloc, hipHostMalloc,
+ * hipStreamCreate); steady-state planning allocates no device memory and
+ * makes no device-synchronizing call.  A pooled buffer's upload first waits,
+ * on `upload_stream`, for the work its previous plan enqueued.  On success
+ * *out is a new plan; on failure *out is NULL.
  * Errors: INVALID_ARG (null pointer, Hq % Hkv != 0, q_len > kv_len, segments
  * not tiling [0, kv_len), negative window, kv_len > 16 * max_blocks_per_seq,
  * overlapping row ranges, ...), UNSUPPORTED (head_dim, page_size, dtype),
  * NOMEM, HIP. */
 int mstar_attn_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                     const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segments,
-                    int32_t num_segs, void* upload_stream, mstar_plan_t** out);
+                    int32_t num_segs, hipStream_t upload_stream, mstar_plan_t** out);
 
 /* mstar_attn_plan with shared-prefix groups (a cascade).  For each group the
  * prefix keys are attended once for the query rows of all members together
@@ -185,41 +192,48 @@ int mstar_attn_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
 int mstar_attn_plan_cascade(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                             const mstar_mask_spec* masks, int32_t num_seqs, const mstar_segment* segments,
                             int32_t num_segs, const mstar_prefix_group* groups, int32_t num_groups,
-                            const int32_t* members, int32_t num_members, void* upload_stream, mstar_plan_t** out);
+                            const int32_t* members, int32_t num_members, hipStream_t upload_stream,
+                            mstar_plan_t** out);
 
 /* Bytes of device scratch fwd needs (fp32 partial outputs and their LSEs for
  * split key ranges); 0 if nothing is split.  Returns 0 for a NULL plan. */
 size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan);
 
-/* Run the planned attention on `stream` (a hipStream_t; NULL = default).
+/* Run the planned attention on `stream` (NULL = default stream): the
+ * batched attention of one node execution, every request of the batch at its
+ * own graph position with its own mask, over K/V read in place from the paged
+ * pool (paged attention of the transformer engine, Sec. 3.3, Runtime; one
+ * replica serving requests of every Walk in one batch, Sec. 3.2; labels and
+ * rollout candidates over shared pages, Sec. 4.1 and 4.4).
  * q, k_pages, v_pages, block_table: caller-owned device memory, read only;
  * pages may be shared between requests.  out, lse: caller-owned device
  * memory, written for every row of every request (rows of no request are
  * untouched).  workspace: caller-owned device memory of at least
  * mstar_attn_workspace_bytes(plan) bytes (may be NULL if that is 0); fwd
- * overwrites it.  Enqueues at most four kernels (multi-row tiles or cascade
- * items, few-row items, fp32 items, then the merge of split key ranges); no
+ * overwrites it.  Enqueues the plan's kernels -- multi-row tiles, few-row
+ * items, shared-prefix cascade items or fp32 items, then the merge of split
+ * key ranges; at most four, three for a plan without prefix groups -- with no
  * allocation, no host synchronization and no host reads, so the call may be
  * captured in a HIP graph.  When a plan has both multi-row tile items and
- * few-row items, the few-row kernel runs beside the tile kernel on a side stream of the
- * calling thread (default priority, created by the thread's first such call
- * outside graph capture and kept until the process ends; inside a capture
- * before it exists the kernels run one after the other): `stream` forks to it
- * and joins back before the merge through two events of the plan, so calls
- * with one plan must not overlap in time (MSTAR_FLAG_SERIAL turns this off).
- * The same plan may run with any
- * tensors of the planned shapes.  Two fwd calls that overlap in time must use
- * different workspaces.  Block-table
- * entries outside [0, num_pages) are never dereferenced: they read as zeros
- * and set MSTAR_DEVERR_PAGE_RANGE in the plan's device error word.
+ * few-row items, the few-row kernel runs beside the tile kernel on the plan's
+ * side stream (default priority, made when the plan was built): `stream`
+ * forks to it and joins back before the merge through two events of the
+ * plan, so calls with one such plan must not overlap in time
+ * (MSTAR_FLAG_SERIAL turns this off).  Outside graph capture fwd also records
+ * an event of the plan on `stream` after its kernels (see
+ * mstar_attn_plan_destroy).  The same plan may run with any tensors of the
+ * planned shapes.  Two fwd calls that overlap in time must use different
+ * workspaces.  Block-table entries outside [0, num_pages) are never
+ * dereferenced: they read as zeros and set MSTAR_DEVERR_PAGE_RANGE in the
+ * plan's device error word.
  * Errors: INVALID_ARG (null tensor pointer, misaligned pointer), WORKSPACE,
  * HIP (launch failure). */
 int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const void* k_pages,
                    const void* v_pages, const int32_t* block_table, void* out, float* lse,
-                   void* workspace, size_t workspace_bytes, void* stream);
+                   void* workspace, size_t workspace_bytes, hipStream_t stream);
 
-/* mstar_attn_fwd, additionally recording caller-created HIP events
- * (hipEvent_t) right before and right after each kernel it enqueues, on the
+/* mstar_attn_fwd, additionally recording caller-created HIP events right
+ * before and right after each kernel it enqueues, on the
  * stream that kernel runs on (`stream`, or the side stream for a few-row
  * kernel beside multi-row work): index 0 = multi-row tile kernel, 1 = few-row kernel, 2 = fp32
  * kernel, 3 = merge kernel, 4 = shared-prefix cascade kernel (arrays of 5
@@ -228,13 +242,13 @@ int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const void* k_pages,
  * timing (profiling); same contract and errors as mstar_attn_fwd. */
 int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, const void* k_pages,
                          const void* v_pages, const int32_t* block_table, void* out, float* lse,
-                         void* workspace, size_t workspace_bytes, void* stream,
-                         void* const* events_before, void* const* events_after);
+                         void* workspace, size_t workspace_bytes, hipStream_t stream,
+                         const hipEvent_t* events_before, const hipEvent_t* events_after);
 
 /* Synchronize `stream`, then read and clear the plan's sticky device error
  * word into *error_bits (MSTAR_DEVERR_* bits; 0 = no error seen).  Returns
  * INVALID_ARG if a bit was set, OK otherwise, HIP on a runtime failure. */
-int mstar_attn_check(mstar_plan_t* plan, void* stream, int32_t* error_bits);
+int mstar_attn_check(mstar_plan_t* plan, hipStream_t stream, int32_t* error_bits);
 
 /* Planner statistics (host side; no device access). */
 int mstar_attn_plan_stats(const mstar_plan_t* plan, mstar_plan_stats* out);
@@ -310,8 +324,8 @@ int mstar_planner_submit_cascade(mstar_planner_t* planner, const mstar_attn_para
                                  const mstar_seq_desc* seqs, const mstar_mask_spec* masks, int32_t num_seqs,
                                  const mstar_segment* segments, int32_t num_segs, const mstar_prefix_group* groups,
                                  int32_t num_groups, const int32_t* members, int32_t num_members);
-int mstar_planner_take(mstar_planner_t* planner, void* stream, mstar_plan_t** out);
-int mstar_attn_plan_wait(const mstar_plan_t* plan, void* stream);
+int mstar_planner_take(mstar_planner_t* planner, hipStream_t stream, mstar_plan_t** out);
+int mstar_attn_plan_wait(const mstar_plan_t* plan, hipStream_t stream);
 void mstar_planner_destroy(mstar_planner_t* planner);
 
 /* Paged KV append: write the step's new key and value rows into their pages
@@ -336,10 +350,15 @@ void mstar_planner_destroy(mstar_planner_t* planner);
  * sees the new rows.  Returns MSTAR_OK (also when the plan has no new rows) or
  * a negative code. */
 int mstar_kv_append(const mstar_plan_t* plan, const void* k_new, const void* v_new, const int32_t* block_table,
-                    void* k_pages, void* v_pages, void* stream);
+                    void* k_pages, void* v_pages, hipStream_t stream);
 
-/* Release the plan (host and device memory).  The caller guarantees no
- * enqueued fwd still uses it.  NULL is ignored. */
+/* Release the plan: its host memory is freed and its device buffers, staging
+ * copy, events and side stream go back to the per-device pool (no HIP call,
+ * no device synchronization).  Work that fwd or kv_append enqueued outside
+ * graph capture may still be running: a later plan that takes the same
+ * buffers waits for it on the device before overwriting them.  A graph that
+ * captured the plan's calls must not be replayed after the plan is
+ * destroyed.  NULL is ignored. */
 void mstar_attn_plan_destroy(mstar_plan_t* plan);
 
 /* Message for the calling thread's last failing call ("" if none). */

@@ -19,7 +19,10 @@ from typing import Optional
 
 import numpy as np
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmstar_attn.so")
+# MSTAR_ATTN_LIB names another build of the same library (the host-only
+# sanitizer build the CPU tests load); by default the in-tree HIP build.
+LIB_PATH = os.environ.get("MSTAR_ATTN_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                            "libmstar_attn.so")
 
 OK = 0
 ERR_INVALID_ARG = -1

@@ -20,18 +20,112 @@
 
 #define MSTAR_EXPORT extern "C" __attribute__((visibility("default")))
 
+namespace {
+
+// Device-side resources of one plan: the device copy of the plan blob, its
+// pinned staging copy, the events that order their reuse, and (for plans that
+// run the few-row kernel beside the tile kernel) a side stream with its fork
+// and join events.  Blocks are pooled per device: a destroyed plan returns its
+// block and later plans take it back, so steady-state planning calls no
+// hipMalloc / hipHostMalloc / hipFree (hipFree would also synchronize the
+// device) and plan destruction makes no HIP call at all.
+struct PlanBlock {
+    int device = -1;
+    size_t bytes = 0;          // capacity of dev and pinned
+    void* dev = nullptr;
+    void* pinned = nullptr;
+    hipEvent_t uploaded = nullptr;  // after the last upload from `pinned`
+    hipEvent_t last_use = nullptr;  // after the last fwd / kv_append enqueued outside graph capture
+    bool uploaded_set = false, last_use_set = false;
+    hipEvent_t ready = nullptr;     // the async planner's upload-done event
+    hipStream_t side = nullptr;     // few-row kernel beside the tile kernel (default priority)
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+
+constexpr size_t kMinBlockBytes = 64 << 10;
+constexpr size_t kPoolMaxBlocks = 64;  // free blocks kept; more are released
+std::mutex g_pool_mu;
+std::vector<PlanBlock*> g_pool;
+
+void free_block(PlanBlock* b) {
+    int cur = 0;
+    const bool have = hipGetDevice(&cur) == hipSuccess;
+    if (hipSetDevice(b->device) == hipSuccess) {
+        if (b->uploaded) (void)hipEventDestroy(b->uploaded);
+        if (b->last_use) (void)hipEventDestroy(b->last_use);
+        if (b->ready) (void)hipEventDestroy(b->ready);
+        if (b->fork) (void)hipEventDestroy(b->fork);
+        if (b->join) (void)hipEventDestroy(b->join);
+        if (b->side) (void)hipStreamDestroy(b->side);
+        if (b->dev) (void)hipFree(b->dev);
+        if (b->pinned) (void)hipHostFree(b->pinned);
+    }
+    if (have) (void)hipSetDevice(cur);
+    delete b;
+}
+
+// A block of at least `bytes` on the current device: the smallest fitting free
+// one, else a new one (capacity rounded up to a power of two).
+hipError_t acquire_block(size_t bytes, PlanBlock** out) {
+    *out = nullptr;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    {
+        std::lock_guard<std::mutex> lk(g_pool_mu);
+        size_t best = g_pool.size();
+        for (size_t i = 0; i < g_pool.size(); ++i)
+            if (g_pool[i]->device == dev && g_pool[i]->bytes >= bytes &&
+                (best == g_pool.size() || g_pool[i]->bytes < g_pool[best]->bytes))
+                best = i;
+        if (best < g_pool.size()) {
+            *out = g_pool[best];
+            g_pool.erase(g_pool.begin() + (ptrdiff_t)best);
+            return hipSuccess;
+        }
+    }
+    PlanBlock* b = new (std::nothrow) PlanBlock();
+    if (!b) return hipErrorOutOfMemory;
+    b->device = dev;
+    size_t cap = kMinBlockBytes;
+    while (cap < bytes) cap <<= 1;
+    b->bytes = cap;
+    if ((e = hipMalloc(&b->dev, cap)) == hipSuccess && (e = hipHostMalloc(&b->pinned, cap, hipHostMallocDefault)) == hipSuccess &&
+        (e = hipEventCreateWithFlags(&b->uploaded, hipEventDisableTiming)) == hipSuccess &&
+        (e = hipEventCreateWithFlags(&b->last_use, hipEventDisableTiming)) == hipSuccess) {
+        *out = b;
+        return hipSuccess;
+    }
+    free_block(b);
+    return e;
+}
+
+void release_block(PlanBlock* b) {
+    if (!b) return;
+    {
+        std::lock_guard<std::mutex> lk(g_pool_mu);
+        if (g_pool.size() < kPoolMaxBlocks) {
+            g_pool.push_back(b);
+            return;
+        }
+    }
+    free_block(b);
+}
+
+}  // namespace
+
 struct mstar_plan {
     mstar::HostPlan host;
-    void* dev = nullptr;     // device copy of the plan blob
-    void* pinned = nullptr;  // pinned staging copy (kept until destroy)
+    PlanBlock* blk = nullptr;  // device resources (NULL for a host-only plan)
+    void* dev = nullptr;       // blk->dev
     size_t bytes = 0;
     size_t off_seqs = 0, off_row_hi = 0, off_tiles = 0, off_order = 0, off_few = 0, off_f32 = 0, off_merge = 0, off_append = 0, off_casc = 0, off_casc_rows = 0, off_casc_order = 0, off_err = 0;
     double plan_us = 0.0;
-    hipEvent_t ready = nullptr;  // recorded after the upload by the async planner
-    // A plan with both tile and few-row items runs the few-row kernel on a
-    // side stream beside the tile kernel: the caller's stream forks at `fork`
-    // and joins at `join` before the merge.
-    hipEvent_t fork = nullptr, join = nullptr;
+    // A plan with both tile and few-row items runs the few-row kernel on
+    // blk->side beside the tile kernel: the caller's stream forks at blk->fork
+    // and joins at blk->join before the merge.
+    bool forked = false;
+    bool from_planner = false;  // built by an async planner: blk->ready marks its upload
 };
 
 namespace {
@@ -49,22 +143,17 @@ int hip_fail(hipError_t e, const char* what) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// The calling thread's side stream on the current device (default priority,
-// non-blocking), created on first use and kept until the process ends; one per
-// thread, so that work forked by different threads (or captured into a graph
-// by one of them) never shares a stream.  It is not created while `main` is
-// being captured into a graph.  nullptr if it cannot be had.
-hipStream_t side_stream(hipStream_t main) {
-    constexpr int kMaxDevices = 64;
-    thread_local hipStream_t streams[kMaxDevices] = {};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
-    if (!streams[dev]) {
-        hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
-        if (hipStreamIsCapturing(main, &st) != hipSuccess || st != hipStreamCaptureStatusNone) return nullptr;
-        if (hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking) != hipSuccess) streams[dev] = nullptr;
-    }
-    return streams[dev];
+// Records that `plan`'s device blob is read by work enqueued on `s` (so that a
+// later plan reusing the block waits for it), unless `s` is being captured
+// into a graph: a capture's replays are the caller's to finish before the
+// plan is destroyed.
+hipError_t mark_use(const mstar_plan* plan, hipStream_t s) {
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    hipError_t e = hipStreamIsCapturing(s, &st);
+    if (e != hipSuccess || st != hipStreamCaptureStatusNone) return e;
+    e = hipEventRecord(plan->blk->last_use, s);
+    if (e == hipSuccess) plan->blk->last_use_set = true;
+    return e;
 }
 
 template <typename T>
@@ -80,7 +169,7 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 static int plan_impl(const mstar_attn_params* params, const mstar_seq_desc* seqs, const mstar_mask_spec* masks,
                      int32_t num_seqs, const mstar_segment* segments, int32_t num_segs,
                      const mstar_prefix_group* groups, int32_t num_groups, const int32_t* members,
-                     int32_t num_members, void* upload_stream, mstar_plan_t** out) {
+                     int32_t num_members, hipStream_t upload_stream, mstar_plan_t** out) {
     const auto t0 = std::chrono::steady_clock::now();
     if (!out) return fail(MSTAR_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
@@ -126,12 +215,26 @@ static int plan_impl(const mstar_attn_params* params, const mstar_seq_desc* seqs
     plan->bytes = off;
 
     if (!host_only) {
-        hipError_t e = hipHostMalloc(&plan->pinned, plan->bytes, hipHostMallocDefault);
+        hipStream_t up = upload_stream;
+        PlanBlock* b = nullptr;
+        hipError_t e = acquire_block(plan->bytes, &b);
         if (e != hipSuccess) {
             delete plan;
-            return hip_fail(e, "hipHostMalloc(plan staging)");
+            return e == hipErrorOutOfMemory ? fail(MSTAR_ERR_NOMEM, "plan buffers: out of memory")
+                                            : hip_fail(e, "plan buffers");
         }
-        unsigned char* blob = static_cast<unsigned char*>(plan->pinned);
+        plan->blk = b;
+        plan->dev = b->dev;
+        auto give_up = [&](hipError_t err, const char* what) {
+            release_block(b);
+            delete plan;
+            return hip_fail(err, what);
+        };
+        // a reused block: its previous upload must have left the staging copy
+        // (normally long done) before the host rewrites it
+        if (b->uploaded_set && (e = hipEventSynchronize(b->uploaded)) != hipSuccess)
+            return give_up(e, "hipEventSynchronize(plan staging)");
+        unsigned char* blob = static_cast<unsigned char*>(b->pinned);
         std::memset(blob, 0, plan->bytes);
         put(blob, plan->off_seqs, h.seqs);
         put(blob, plan->off_row_hi, h.row_hi);
@@ -144,28 +247,33 @@ static int plan_impl(const mstar_attn_params* params, const mstar_seq_desc* seqs
         put(blob, plan->off_casc, h.cascade);
         put(blob, plan->off_casc_rows, h.casc_rows);
         put(blob, plan->off_casc_order, h.casc_order);
-        e = hipMalloc(&plan->dev, plan->bytes);
-        if (e != hipSuccess) {
-            (void)hipHostFree(plan->pinned);
-            delete plan;
-            return hip_fail(e, "hipMalloc(plan)");
-        }
-        e = hipMemcpyAsync(plan->dev, plan->pinned, plan->bytes, hipMemcpyHostToDevice,
-                           static_cast<hipStream_t>(upload_stream));
+        // ... and work of the block's previous plan that reads the device copy
+        // must be done before the upload overwrites it (a device-side wait)
+        if (b->last_use_set && (e = hipStreamWaitEvent(up, b->last_use, 0)) != hipSuccess)
+            return give_up(e, "hipStreamWaitEvent(plan reuse)");
+        if ((e = hipMemcpyAsync(b->dev, b->pinned, plan->bytes, hipMemcpyHostToDevice, up)) != hipSuccess)
+            return give_up(e, "plan upload");
+        if ((e = hipEventRecord(b->uploaded, up)) != hipSuccess) return give_up(e, "hipEventRecord(plan upload)");
+        b->uploaded_set = true;
         // the few-row kernel goes beside the tile kernel (prefill work), not
         // beside the cascade kernel, whose L2-fed prefix tiles and the few-row
-        // kernel's HBM stream slow each other down more than they overlap
-        if (e == hipSuccess && !h.tiles.empty() && !h.few.empty() && !(p.flags & MSTAR_FLAG_SERIAL)) {
-            e = hipEventCreateWithFlags(&plan->fork, hipEventDisableTiming);
-            if (e == hipSuccess) e = hipEventCreateWithFlags(&plan->join, hipEventDisableTiming);
-        }
-        if (e != hipSuccess) {
-            if (plan->fork) (void)hipEventDestroy(plan->fork);
-            if (plan->join) (void)hipEventDestroy(plan->join);
-            (void)hipFree(plan->dev);
-            (void)hipHostFree(plan->pinned);
-            delete plan;
-            return hip_fail(e, "plan upload");
+        // kernel's HBM stream slow each other down more than they overlap;
+        // the side stream and its events are made here (once per block), not
+        // in fwd
+        if (!h.tiles.empty() && !h.few.empty() && !(p.flags & MSTAR_FLAG_SERIAL)) {
+            if (!b->side && (e = hipStreamCreateWithFlags(&b->side, hipStreamNonBlocking)) != hipSuccess) {
+                b->side = nullptr;
+                return give_up(e, "side stream");
+            }
+            if (!b->fork && (e = hipEventCreateWithFlags(&b->fork, hipEventDisableTiming)) != hipSuccess) {
+                b->fork = nullptr;
+                return give_up(e, "fork event");
+            }
+            if (!b->join && (e = hipEventCreateWithFlags(&b->join, hipEventDisableTiming)) != hipSuccess) {
+                b->join = nullptr;
+                return give_up(e, "join event");
+            }
+            plan->forked = true;
         }
     }
     plan->plan_us = std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
@@ -175,7 +283,7 @@ static int plan_impl(const mstar_attn_params* params, const mstar_seq_desc* seqs
 
 MSTAR_EXPORT int mstar_attn_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                                  const mstar_mask_spec* masks, int32_t num_seqs,
-                                 const mstar_segment* segments, int32_t num_segs, void* upload_stream,
+                                 const mstar_segment* segments, int32_t num_segs, hipStream_t upload_stream,
                                  mstar_plan_t** out) {
     return plan_impl(params, seqs, masks, num_seqs, segments, num_segs, nullptr, 0, nullptr, 0, upload_stream, out);
 }
@@ -184,7 +292,7 @@ MSTAR_EXPORT int mstar_attn_plan_cascade(const mstar_attn_params* params, const 
                                          const mstar_mask_spec* masks, int32_t num_seqs,
                                          const mstar_segment* segments, int32_t num_segs,
                                          const mstar_prefix_group* groups, int32_t num_groups,
-                                         const int32_t* members, int32_t num_members, void* upload_stream,
+                                         const int32_t* members, int32_t num_members, hipStream_t upload_stream,
                                          mstar_plan_t** out) {
     return plan_impl(params, seqs, masks, num_seqs, segments, num_segs, groups, num_groups, members, num_members,
                      upload_stream, out);
@@ -198,15 +306,15 @@ MSTAR_EXPORT size_t mstar_attn_workspace_bytes(const mstar_plan_t* plan) {
 
 MSTAR_EXPORT int mstar_attn_fwd(const mstar_plan_t* plan, const void* q, const void* k_pages,
                                 const void* v_pages, const int32_t* block_table, void* out, float* lse,
-                                void* workspace, size_t workspace_bytes, void* stream) {
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
     return mstar_attn_fwd_timed(plan, q, k_pages, v_pages, block_table, out, lse, workspace, workspace_bytes,
                                 stream, nullptr, nullptr);
 }
 
 MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, const void* k_pages,
                                       const void* v_pages, const int32_t* block_table, void* out, float* lse,
-                                      void* workspace, size_t workspace_bytes, void* stream,
-                                      void* const* events_before, void* const* events_after) {
+                                      void* workspace, size_t workspace_bytes, hipStream_t stream,
+                                      const hipEvent_t* events_before, const hipEvent_t* events_after) {
     if (!plan) return fail(MSTAR_ERR_INVALID_ARG, "plan is NULL");
     if (!plan->dev) return fail(MSTAR_ERR_INVALID_ARG, "plan was built host-only");
     const mstar::HostPlan& h = plan->host;
@@ -244,24 +352,25 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
     a.num_pages = h.params.num_pages;
     a.sm_scale = h.params.sm_scale;
     a.scale_log2 = h.params.sm_scale * 1.4426950408889634f;
-    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipStream_t s = stream;
 
     hipError_t e;
     // The few-row kernel runs on the thread's side stream when the plan also
     // has tile work: it streams K/V from HBM while the tile kernel keeps the
     // matrix units busy.  Both write disjoint outputs and partial slots; the
     // merge waits for both.
-    hipStream_t side = plan->fork ? side_stream(s) : nullptr;
+    PlanBlock* b = plan->blk;
+    hipStream_t side = plan->forked ? b->side : nullptr;
     if (side) {
-        if ((e = hipEventRecord(plan->fork, s)) != hipSuccess) return hip_fail(e, "hipEventRecord(fork)");
-        if ((e = hipStreamWaitEvent(side, plan->fork, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(fork)");
+        if ((e = hipEventRecord(b->fork, s)) != hipSuccess) return hip_fail(e, "hipEventRecord(fork)");
+        if ((e = hipStreamWaitEvent(side, b->fork, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(fork)");
     }
     hipStream_t s_few = side ? side : s;
     // optional HIP events around kernel class k (0 tiles, 1 few-row, 2 fp32, 3 merge, 4 cascade),
     // recorded on the stream that kernel runs on
-    auto mark = [&](void* const* evs, int k) -> hipError_t {
+    auto mark = [&](const hipEvent_t* evs, int k) -> hipError_t {
         if (!evs || !evs[k]) return hipSuccess;
-        return hipEventRecord(static_cast<hipEvent_t>(evs[k]), k == 1 ? s_few : s);
+        return hipEventRecord(evs[k], k == 1 ? s_few : s);
     };
 #define MSTAR_MARK(evs, k) \
     if ((e = mark(evs, k)) != hipSuccess) return hip_fail(e, "hipEventRecord")
@@ -273,7 +382,7 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
         MSTAR_MARK(events_after, 1);
     }
     if (side) {
-        if ((e = hipEventRecord(plan->join, side)) != hipSuccess) return hip_fail(e, "hipEventRecord(join)");
+        if ((e = hipEventRecord(b->join, side)) != hipSuccess) return hip_fail(e, "hipEventRecord(join)");
     }
     if (!h.tiles.empty()) {
         a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_tiles);
@@ -295,7 +404,7 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
         MSTAR_MARK(events_after, 4);
     }
     if (side) {
-        if ((e = hipStreamWaitEvent(s, plan->join, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(join)");
+        if ((e = hipStreamWaitEvent(s, b->join, 0)) != hipSuccess) return hip_fail(e, "hipStreamWaitEvent(join)");
     }
     if (!h.f32.empty()) {
         a.items = reinterpret_cast<const mstar::WorkItem*>(blob + plan->off_f32);
@@ -319,11 +428,12 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
         MSTAR_MARK(events_after, 3);
     }
 #undef MSTAR_MARK
+    if ((e = mark_use(plan, s)) != hipSuccess) return hip_fail(e, "hipEventRecord(plan use)");
     return MSTAR_OK;
 }
 
 MSTAR_EXPORT int mstar_kv_append(const mstar_plan_t* plan, const void* k_new, const void* v_new,
-                                 const int32_t* block_table, void* k_pages, void* v_pages, void* stream) {
+                                 const int32_t* block_table, void* k_pages, void* v_pages, hipStream_t stream) {
     if (!plan) return fail(MSTAR_ERR_INVALID_ARG, "plan is NULL");
     if (!plan->dev) return fail(MSTAR_ERR_INVALID_ARG, "plan was built host-only");
     const mstar::HostPlan& h = plan->host;
@@ -348,16 +458,18 @@ MSTAR_EXPORT int mstar_kv_append(const mstar_plan_t* plan, const void* k_new, co
     a.row_bytes = h.params.num_kv_heads * h.params.head_dim * elt;
     a.bt_stride = h.params.max_blocks_per_seq;
     a.num_pages = h.params.num_pages;
-    hipError_t e = mstar::launch_append(a, static_cast<hipStream_t>(stream));
+    hipError_t e = mstar::launch_append(a, stream);
     if (e != hipSuccess) return hip_fail(e, "append kernel launch");
+    if ((e = mark_use(plan, stream)) != hipSuccess)
+        return hip_fail(e, "hipEventRecord(plan use)");
     return MSTAR_OK;
 }
 
-MSTAR_EXPORT int mstar_attn_check(mstar_plan_t* plan, void* stream, int32_t* error_bits) {
+MSTAR_EXPORT int mstar_attn_check(mstar_plan_t* plan, hipStream_t stream, int32_t* error_bits) {
     if (!plan || !error_bits) return fail(MSTAR_ERR_INVALID_ARG, "plan or error_bits is NULL");
     *error_bits = 0;
     if (!plan->dev) return MSTAR_OK;
-    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipStream_t s = stream;
     hipError_t e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
     int32_t* d_err = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(plan->dev) + plan->off_err);
@@ -453,11 +565,7 @@ MSTAR_EXPORT int mstar_attn_plan_cascade_order(const mstar_plan_t* plan, int32_t
 
 MSTAR_EXPORT void mstar_attn_plan_destroy(mstar_plan_t* plan) {
     if (!plan) return;
-    if (plan->ready) (void)hipEventDestroy(plan->ready);
-    if (plan->fork) (void)hipEventDestroy(plan->fork);
-    if (plan->join) (void)hipEventDestroy(plan->join);
-    if (plan->dev) (void)hipFree(plan->dev);
-    if (plan->pinned) (void)hipHostFree(plan->pinned);
+    release_block(plan->blk);  // back to the pool: no HIP call, no device synchronization
     delete plan;
 }
 
@@ -485,6 +593,7 @@ struct mstar_planner {
         int rc = MSTAR_OK;
         std::string err;
         mstar_plan_t* plan = nullptr;
+        bool planner_built = false;
     };
     std::mutex mu;
     std::condition_variable cv_work, cv_done, cv_space;
@@ -510,7 +619,7 @@ struct mstar_planner {
             Done d;
             d.id = job.id;
             const bool host_only = (job.p.flags & MSTAR_FLAG_HOST_ONLY) != 0;
-            void* s = nullptr;
+            hipStream_t s = nullptr;
             if (!host_only) {
                 hipError_t e = hipSetDevice(job.device);
                 if (e == hipSuccess && (!stream || stream_device != job.device)) {
@@ -533,17 +642,16 @@ struct mstar_planner {
                 if (d.rc != MSTAR_OK) {
                     d.err = mstar_last_error();
                 } else if (!host_only) {
-                    hipEvent_t ev = nullptr;
-                    hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
-                    if (e == hipSuccess) e = hipEventRecord(ev, stream);
+                    PlanBlock* b = d.plan->blk;
+                    hipError_t e = b->ready ? hipSuccess : hipEventCreateWithFlags(&b->ready, hipEventDisableTiming);
+                    if (e == hipSuccess) e = hipEventRecord(b->ready, stream);
                     if (e != hipSuccess) {
-                        if (ev) (void)hipEventDestroy(ev);
                         mstar_attn_plan_destroy(d.plan);
                         d.plan = nullptr;
                         d.rc = MSTAR_ERR_HIP;
                         d.err = std::string("async planner event: ") + hipGetErrorString(e);
                     } else {
-                        d.plan->ready = ev;
+                        d.planner_built = true;
                     }
                 }
             }
@@ -617,7 +725,7 @@ MSTAR_EXPORT int mstar_planner_submit(mstar_planner_t* planner, const mstar_attn
                                         nullptr, 0);
 }
 
-MSTAR_EXPORT int mstar_planner_take(mstar_planner_t* planner, void* stream, mstar_plan_t** out) {
+MSTAR_EXPORT int mstar_planner_take(mstar_planner_t* planner, hipStream_t stream, mstar_plan_t** out) {
     if (!planner || !out) return fail(MSTAR_ERR_INVALID_ARG, "planner or out is NULL");
     *out = nullptr;
     mstar_planner::Done d;
@@ -633,8 +741,9 @@ MSTAR_EXPORT int mstar_planner_take(mstar_planner_t* planner, void* stream, msta
     }
     planner->cv_space.notify_one();
     if (d.rc != MSTAR_OK) return fail(d.rc, d.err);
-    if (d.plan->ready && stream) {
-        hipError_t e = hipStreamWaitEvent(static_cast<hipStream_t>(stream), d.plan->ready, 0);
+    if (d.planner_built) d.plan->from_planner = true;
+    if (d.plan->from_planner && stream) {
+        hipError_t e = hipStreamWaitEvent(stream, d.plan->blk->ready, 0);
         if (e != hipSuccess) {
             mstar_attn_plan_destroy(d.plan);
             return hip_fail(e, "hipStreamWaitEvent(plan upload)");
@@ -644,10 +753,10 @@ MSTAR_EXPORT int mstar_planner_take(mstar_planner_t* planner, void* stream, msta
     return MSTAR_OK;
 }
 
-MSTAR_EXPORT int mstar_attn_plan_wait(const mstar_plan_t* plan, void* stream) {
+MSTAR_EXPORT int mstar_attn_plan_wait(const mstar_plan_t* plan, hipStream_t stream) {
     if (!plan) return fail(MSTAR_ERR_INVALID_ARG, "plan is NULL");
-    if (!plan->ready) return MSTAR_OK;
-    hipError_t e = hipStreamWaitEvent(static_cast<hipStream_t>(stream), plan->ready, 0);
+    if (!plan->from_planner) return MSTAR_OK;
+    hipError_t e = hipStreamWaitEvent(stream, plan->blk->ready, 0);
     return e == hipSuccess ? MSTAR_OK : hip_fail(e, "hipStreamWaitEvent(plan upload)");
 }
 

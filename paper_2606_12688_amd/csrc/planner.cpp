@@ -310,6 +310,10 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
 
     // ---- 3. work units ----------------------------------------------------
     std::vector<Unit> few_units, tile_units;
+    // (request, first row, rows) of member row tiles whose rows see no key past
+    // the shared prefix: their outputs come from the prefix partials alone
+    struct RowRun { int32_t seq, row0, nrows; };
+    std::vector<RowRun> prefix_only;
     for (int32_t r = 0; r < num_seqs; ++r) {
         const mstar_seq_desc& s = seqs[r];
         if (s.q_len == 0) continue;
@@ -338,6 +342,9 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                     const int32_t nr = std::min<int32_t>(span, (int32_t)R - rr0);
                     const int32_t q0 = rr0 / G, q1 = (rr0 + nr - 1) / G;
                     Unit u{r, kvh, rr0, nr, member ? own0 : align_down16(v.lo[q0]), v.hi[q1], 0};
+                    // a member unit whose rows see only the prefix keeps an
+                    // empty own range (it writes empty partials for the merge)
+                    u.k_end = std::max(u.k_end, u.k_begin);
                     u.cost = (int64_t)(u.k_end - u.k_begin);
                     u.partial = member;
                     few_units.push_back(u);
@@ -350,7 +357,10 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                 const int32_t nr = std::min(kTileRows, s.q_len - row0);
                 const int32_t kb = member ? own0 : align_down16(v.lo[row0]);
                 const int32_t ke = v.hi[row0 + nr - 1];
-                if (ke <= kb) continue;  // rows that see only the prefix
+                if (ke <= kb) {  // rows that see only the prefix (members only: kb = 0 otherwise)
+                    if (member) prefix_only.push_back({r, row0, nr});
+                    continue;
+                }
                 Unit u{r, -1, row0, nr, kb, ke, 0};
                 u.partial = member;
                 tile_units.push_back(u);
@@ -433,11 +443,11 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         m.pad1 = (int32_t)cslot.rows;
         m.pad2 = (int32_t)cslot.chunks;
     };
-    // members that see nothing past the prefix: the merge reads the prefix partials alone
-    for (int32_t r = 0; r < num_seqs; ++r) {
-        if (group_of[r] < 0 || seqs[r].q_len == 0) continue;
-        if (iv[r].hi[seqs[r].q_len - 1] > groups[group_of[r]].prefix_len) continue;
-        for (int32_t i = 0; i < seqs[r].q_len; ++i)
+    // member rows that see nothing past the prefix (a whole request, or the
+    // row tiles of one whose first rows sit inside the prefix's block): the
+    // merge reads the prefix partials alone
+    auto prefix_only_rows = [&](int32_t r, int32_t i0, int32_t i1) {
+        for (int32_t i = i0; i < i1; ++i)
             for (int32_t h = 0; h < P.num_qo_heads; ++h) {
                 MergeItem m;
                 m.row = seqs[r].q_start + i;
@@ -448,7 +458,13 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                 prefix_slots(m, r, i, h);
                 plan.merges.push_back(m);
             }
+    };
+    for (int32_t r = 0; r < num_seqs; ++r) {
+        if (group_of[r] < 0 || seqs[r].q_len == 0) continue;
+        if (iv[r].hi[seqs[r].q_len - 1] > groups[group_of[r]].prefix_len) continue;
+        prefix_only_rows(r, 0, seqs[r].q_len);
     }
+    for (const RowRun& run : prefix_only) prefix_only_rows(run.seq, run.row0, run.row0 + run.nrows);
     // Few-row units are cut into pieces of exactly `chunk` keys plus one shorter
     // remainder: with longest-first order the equal pieces fill every CU evenly
     // and the remainders fill the gaps (a simulation of the decode batch on 256

@@ -262,7 +262,8 @@ def test_cascade_launch_order_spreads_one_group_over_every_xcd():
     pl.destroy()
 
 
-CASCADE = ["rollout_bf16", "cfg_labels_bf16", "mixed", "shared_prefix_decode_bf16", "serving_mix_bf16"]
+CASCADE = ["rollout_bf16", "cfg_labels_bf16", "mixed", "shared_prefix_decode_bf16", "serving_mix_bf16",
+           "queried_prefix_bf16"]
 
 
 @pytest.mark.parametrize("name", CASCADE)
@@ -333,6 +334,20 @@ def test_cascade_plan_covers_each_visible_pair_once_and_merges_read_written_slot
     for (req, i, h) in cover:  # every member output is merged
         if req in members:
             assert (req, i, h) in merged
+    # every output has exactly one writer: a final item or a merge record
+    finals = set()
+    for kind in (0, 1):
+        for seq, head, row0, nrows, kb, ke, part, hs in pl.items(kind):
+            if part >= 0:
+                continue
+            for h in (range(b.num_qo_heads) if kind == 0 else [head]):
+                for r in range(nrows):
+                    rr = row0 + r
+                    finals.add((seq, rr // G, h * G + rr % G) if kind == 1 else (seq, rr, h))
+    for r in range(b.num_seqs):
+        for i in range(int(b.seqs[r, 0])):
+            for h in range(b.num_qo_heads):
+                assert ((r, i, h) in finals) != ((r, i, h) in merged), (r, i, h)
     pl.destroy()
 
 

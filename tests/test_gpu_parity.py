@@ -6,42 +6,22 @@ import numpy as np
 import pytest
 
 import workloads as W
-from oracle import oracle_attention, oracle_rows
+from oracle import oracle_rows
 from paper_2606_12688_amd import attn
-from tests.helpers import plan_for, run_gpu
+from tests.helpers import TOL, compare, host64, oracle_of, plan_for, run_gpu
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
-TOL = {"f32": (1e-5, 1e-3), "bf16": (1.5e-2, 1e-3)}
-
-
-def _host(t):
-    return t.float().cpu().numpy().astype(np.float64)
-
-
-def _compare(b, out, lse, ref_o, ref_l, label="", rel_o=0.0):
-    """Max-abs errors against the bars above; rel_o widens the output bar by
-    rel_o * |reference| (for outputs far from unit size, see its caller)."""
-    tol_o, tol_l = TOL[b.dtype]
-    o = _host(out)
-    l = lse.cpu().numpy().astype(np.float64)
-    assert np.isfinite(o).all(), f"{label}: non-finite output"
-    assert np.isfinite(l).all(), f"{label}: non-finite lse"
-    eo = float((np.abs(o - ref_o) - rel_o * np.abs(ref_o)).max()) if o.size else 0.0
-    el = float(np.abs(l - ref_l).max()) if l.size else 0.0
-    print(f"{label}: max|dout|={eo:.3e} max|dlse|={el:.3e}", flush=True)
-    assert eo <= tol_o, f"{label}: out error {eo} > {tol_o}"
-    assert el <= tol_l, f"{label}: lse error {el} > {tol_l}"
-
-
-def _oracle(b, t):
-    h = {k: _host(v) for k, v in t.items()}
-    return oracle_attention(b, h["q"], h["k_pages"], h["v_pages"])
+_host = host64
+_compare = compare
+_oracle = oracle_of
 
 
 REDUCED = ["tiny_causal_f32", "decode_bf16", "text_latent_bf16", "stream_window_bf16", "rollout_bf16",
-           "cfg_labels_bf16", "shared_prefix_decode_bf16", "serving_mix_bf16", "mixed"]
-CASCADE = ["rollout_bf16", "cfg_labels_bf16", "shared_prefix_decode_bf16", "serving_mix_bf16", "mixed"]
+           "cfg_labels_bf16", "shared_prefix_decode_bf16", "serving_mix_bf16", "mixed", "window_edges_bf16",
+           "queried_prefix_bf16"]
+CASCADE = ["rollout_bf16", "cfg_labels_bf16", "shared_prefix_decode_bf16", "serving_mix_bf16", "mixed",
+           "queried_prefix_bf16"]
 FLAGS = {"auto": 0, "force_split": attn.FLAG_FORCE_SPLIT, "no_split": attn.FLAG_NO_SPLIT}
 
 

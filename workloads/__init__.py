@@ -31,6 +31,9 @@ per-layer attention shapes and its datasets are not used):
 * ``shared_prefix_decode_bf16`` - one new token for each of many requests over
                           one shared context plus their own tokens (candidates
                           continued from one context, App. A).
+* ``queried_prefix_bf16`` - requests over a shared full-attention prefix whose
+                          first query rows lie inside that prefix (a shared-
+                          prefix group where some rows see only the prefix).
 * ``mixed``             - requests of all the kinds above in one launch (one
                           ``LLM`` replica serving every Walk, Sec. 3.2).
 
@@ -278,6 +281,26 @@ def cfg_labels_bf16(seed: int = 0, n: int = 2, text: int = 256, image: int = 409
     return b
 
 
+def queried_prefix_bf16(seed: int = 0, n: int = 4, prefix: int = 2048, tail: int = 256, q: int = 400,
+                        hq: int = 8, hkv: int = 2, d: int = 128) -> Batch:
+    """n requests over one shared ``prefix`` (one full-attention block whose
+    pages every block table points to) followed by ``tail`` causal tokens of
+    their own; the last ``q`` positions are queried, so the first query rows lie
+    inside the prefix's block (they see exactly the prefix) and the rest see the
+    prefix plus their causal tail.  One prefix group holds every request."""
+    if prefix % PAGE:
+        raise ValueError("shared prefix must be page aligned")
+    L = prefix + tail
+    if not tail < q <= L:
+        raise ValueError("the queried rows must start inside the prefix")
+    kv = [L] * n
+    bt, pool = _layout_pages(kv, None, _rng(seed, _SUB_PERM), shared_prefix_pages=prefix // PAGE)
+    segs = [[(0, prefix, SEG_FULL, 0), (prefix, tail, SEG_CAUSAL, 0)] for _ in range(n)]
+    b = _finish("queried_prefix_bf16", hq, hkv, d, "bf16", [q] * n, kv, segs, [0] * n, bt, pool, seed)
+    b.prefix_groups = [(list(range(n)), prefix)]
+    return b
+
+
 def mixed(seed: int = 0, hq: int = 8, hkv: int = 2, d: int = 128, dtype: str = "bf16",
           scale: int = 1) -> Batch:
     """Requests of every kind in one launch: decode, text+latent prefill,
@@ -379,6 +402,61 @@ def serving_mix_bf16(seed: int = 0, n_decode: int = 48, lmin: int = 512, lmax: i
     return b
 
 
+def custom(name: str, hq: int, hkv: int, d: int, q_lens, kv_lens, seg_lists, windows, seed: int = 0,
+           dtype: str = "bf16", pool_pages: Optional[int] = None, shared_prefix_pages: int = 0) -> Batch:
+    """A batch from explicit per-request lengths, segment lists and windows,
+    laid out in a seeded permutation of the pool (the first
+    ``shared_prefix_pages`` pages shared by every request)."""
+    bt, pool = _layout_pages(kv_lens, pool_pages, _rng(seed, _SUB_PERM), shared_prefix_pages)
+    return _finish(name, hq, hkv, d, dtype, list(q_lens), list(kv_lens), seg_lists, list(windows), bt, pool, seed)
+
+
+def window_edges_bf16(seed: int = 0, d: int = 128, hq: int = 16, hkv: int = 8) -> Batch:
+    """Sliding windows at their small edges (1 key, fewer keys than a page,
+    exactly a page, one more) on every query shape: single-token decode and
+    16-token chunks (few-row path) and 300-row prefills (tile path) under
+    causal, full-block and block-causal segments, next to windows wider than
+    the context."""
+    q_lens, kv_lens, seg_lists, windows = [], [], [], []
+    rng = _rng(seed, _SUB_LENGTHS)
+    for w in (1, 5, 16, 17):
+        for q, ctx in ((1, int(rng.integers(40, 900))), (16, int(rng.integers(0, 700)))):
+            L = ctx + q
+            q_lens.append(q); kv_lens.append(L); seg_lists.append([(0, L, SEG_CAUSAL, 0)]); windows.append(w)
+        L = 300 + int(rng.integers(0, 400))
+        q_lens.append(300); kv_lens.append(L); seg_lists.append([(0, L, SEG_CAUSAL, 0)]); windows.append(w)
+        # full block after a causal head: rows in the block see later keys of it
+        q_lens.append(300); kv_lens.append(340)
+        seg_lists.append([(0, 40, SEG_CAUSAL, 0), (40, 300, SEG_FULL, 0)]); windows.append(w)
+        # frame blocks of 48 with a ragged last one
+        q_lens.append(250); kv_lens.append(307)
+        seg_lists.append([(0, 19, SEG_CAUSAL, 0), (19, 288, SEG_BLOCKS, 48)]); windows.append(w)
+    # windows wider than the whole context
+    q_lens.append(16); kv_lens.append(116); seg_lists.append([(0, 116, SEG_CAUSAL, 0)]); windows.append(5000)
+    q_lens.append(300); kv_lens.append(300); seg_lists.append([(0, 300, SEG_CAUSAL, 0)]); windows.append(300)
+    return custom("window_edges_bf16", hq, hkv, d, q_lens, kv_lens, seg_lists, windows, seed)
+
+
+def long_items(name: str, seed: int = 0) -> Batch:
+    """Small batches whose single work items are long: tile items over 2048
+    keys (the tile kernel's page-index ring refills its third window) and
+    few-row items over 4096 keys (a wave's page indices span more than one
+    register window).  Planned without key splitting, each request's range
+    stays one item."""
+    if name == "text_latent_long":
+        return text_latent_bf16(seed, n=2, text=64, latent=2500, hq=4, hkv=1)
+    if name == "rollout_long":
+        return rollout_bf16(seed, n=2, prefix=2048, frames=2, frame=128, hq=4, hkv=4, d=64)
+    if name == "decode_long":
+        return decode_bf16(seed, n=8, lmin=6000, lmax=9000, hq=8, hkv=2, pool_pages=None)
+    if name == "chunk_long":
+        return stream_window_bf16(seed, n=4, cmin=6000, cmax=9000, window=5000, hq=8, hkv=4)
+    raise KeyError(name)
+
+
+LONG_ITEMS = ["text_latent_long", "rollout_long", "decode_long", "chunk_long"]
+
+
 FULL_SIZE = {
     "tiny_causal_f32": tiny_causal_f32,
     "decode_bf16": decode_bf16,
@@ -414,6 +492,10 @@ def reduced(name: str, seed: int = 0) -> Batch:
                                 cmax=600, window=96, n_roll=3, prefix=64, frames=2, frame=40, hq=7, hkv=1)
     if name == "mixed":
         return mixed(seed)
+    if name == "window_edges_bf16":
+        return window_edges_bf16(seed)
+    if name == "queried_prefix_bf16":
+        return queried_prefix_bf16(seed, n=3, prefix=192, tail=64, q=200, hq=4, hkv=1, d=64)
     raise KeyError(name)
 
 
@@ -509,18 +591,26 @@ def _as_index(x, idx):
     return torch.from_numpy(idx.astype(np.int64)).to(x.device)
 
 
-def extract_requests(b: Batch, tensors: dict, reqs, to_host=None):
+def extract_requests(b: Batch, tensors: dict, reqs, to_host=None, key_ranges=None):
     """The requests ``reqs`` of ``b`` as a batch of their own, with only their
     pages (renumbered) and their query rows.  ``tensors`` may live on any
     device; ``to_host`` converts a tensor to a float64 numpy array (default:
-    ``.float().cpu().numpy()``).  Returns ``(sub_batch, q, k_pages, v_pages,
-    rows)`` where ``rows`` are the packed query rows of the originals."""
+    ``.float().cpu().numpy()``).  With ``key_ranges`` (one ``(lo, hi)`` per
+    selected request, covering every key its rows may see) only the pages
+    holding those keys are copied and the other block-table entries become
+    -1.  Returns ``(sub_batch, q, k_pages, v_pages, rows)`` where ``rows`` are
+    the packed query rows of the originals."""
     reqs = [int(r) for r in reqs]
     if to_host is None:
         def to_host(t):
             return np.asarray(t.float().cpu().numpy(), dtype=np.float64) if not isinstance(t, np.ndarray) \
                 else np.asarray(t, dtype=np.float64)
-    bt = b.block_table[reqs]
+    bt = b.block_table[reqs].copy()
+    if key_ranges is not None:
+        for j, (lo, hi) in enumerate(key_ranges):
+            keep = np.zeros(bt.shape[1], dtype=bool)
+            keep[int(lo) // b.page_size:(int(hi) + b.page_size - 1) // b.page_size] = True
+            bt[j, ~keep] = -1
     pages = np.unique(bt[bt >= 0])
     nbt = np.where(bt >= 0, np.searchsorted(pages, bt), -1).astype(np.int32)
     seqs = b.seqs[reqs].copy()
