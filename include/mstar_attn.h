@@ -245,6 +245,26 @@ int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, const void* k_
                          void* workspace, size_t workspace_bytes, hipStream_t stream,
                          const hipEvent_t* events_before, const hipEvent_t* events_after);
 
+/* mstar_attn_fwd without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the split-K partials go to a static
+ * device array of MSTAR_NOALLOC_SCRATCH_BYTES held by the library on each GPU
+ * it runs on until the process ends.  The call allocates nothing (no
+ * hipMalloc, no allocating library routine); its first call on a device looks
+ * up that device's array address once.  The caller still passes inputs and
+ * outputs; plan, tensors, stream and errors as for mstar_attn_fwd.  Returns
+ * MSTAR_ERR_WORKSPACE, without enqueuing anything, if the plan needs more
+ * scratch than the array holds (mstar_attn_workspace_bytes(plan) >
+ * MSTAR_NOALLOC_SCRATCH_BYTES).  Every call on one GPU shares that GPU's
+ * array and leaves its contents behind: nothing in it needs to start at
+ * zero (every partial a merge reads is written by the same call), but two
+ * calls whose kernels overlap in time on one GPU (different streams, or
+ * threads) race on it and must not be issued. */
+#define MSTAR_NOALLOC_SCRATCH_BYTES (32u << 20)
+int mstar_attn_fwd_noalloc(const mstar_plan_t* plan, const void* q, const void* k_pages,
+                           const void* v_pages, const int32_t* block_table, void* out, float* lse,
+                           hipStream_t stream);
+
 /* Synchronize `stream`, then read and clear the plan's sticky device error
  * word into *error_bits (MSTAR_DEVERR_* bits; 0 = no error seen).  Returns
  * INVALID_ARG if a bit was set, OK otherwise, HIP on a runtime failure. */

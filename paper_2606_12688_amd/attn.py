@@ -3,7 +3,8 @@
 Argument marshalling only: every step of the computation runs in the HIP
 library.  PyTorch supplies device memory and streams.  The names follow the C
 entry points: :func:`plan` (``mstar_attn_plan``), :meth:`Plan.workspace_bytes`,
-:func:`fwd` (``mstar_attn_fwd``), :func:`kv_append` (``mstar_kv_append``),
+:func:`fwd` (``mstar_attn_fwd``), :func:`fwd_noalloc` (``mstar_attn_fwd_noalloc``),
+:func:`kv_append` (``mstar_kv_append``),
 :func:`check` (``mstar_attn_check``),
 :class:`AsyncPlanner` (``mstar_planner_*``), :meth:`Plan.stats`, :meth:`Plan.key_ranges`, :meth:`Plan.items`,
 :meth:`Plan.destroy` and :func:`last_error`.
@@ -42,6 +43,7 @@ EXPORTS = [
     "mstar_attn_workspace_bytes",
     "mstar_attn_fwd",
     "mstar_attn_fwd_timed",
+    "mstar_attn_fwd_noalloc",
     "mstar_attn_check",
     "mstar_attn_plan_stats",
     "mstar_attn_plan_key_ranges",
@@ -122,6 +124,8 @@ def lib() -> ctypes.CDLL:
     L.mstar_attn_fwd.restype = ctypes.c_int
     L.mstar_attn_fwd_timed.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp, vp, vp]
     L.mstar_attn_fwd_timed.restype = ctypes.c_int
+    L.mstar_attn_fwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+    L.mstar_attn_fwd_noalloc.restype = ctypes.c_int
     L.mstar_attn_check.argtypes = [vp, vp, ctypes.POINTER(i32)]
     L.mstar_attn_check.restype = ctypes.c_int
     L.mstar_attn_plan_stats.argtypes = [vp, ctypes.POINTER(PlanStats)]
@@ -352,9 +356,9 @@ def _need(cond, msg):
         raise ValueError(msg)
 
 
-def fwd(pl: Plan, q, k_pages, v_pages, block_table, out, lse, workspace=None, stream=None):
-    """``mstar_attn_fwd`` on torch tensors (checks shapes, dtypes and devices so
-    that the kernels never read outside the tensors)."""
+def _check_fwd_tensors(pl: Plan, q, k_pages, v_pages, block_table, out, lse):
+    """Shapes, dtypes and devices, so that the kernels never read outside the
+    tensors."""
     import torch
 
     p = pl.params
@@ -373,6 +377,12 @@ def fwd(pl: Plan, q, k_pages, v_pages, block_table, out, lse, workspace=None, st
     _need(tuple(k_pages.shape) == kv_shape and tuple(v_pages.shape) == kv_shape, f"pages must be {kv_shape}")
     _need(block_table.dtype == torch.int32 and tuple(block_table.shape) == (pl.num_seqs, p.max_blocks_per_seq),
           f"block_table must be int32 [{pl.num_seqs}, {p.max_blocks_per_seq}]")
+    return dev
+
+
+def fwd(pl: Plan, q, k_pages, v_pages, block_table, out, lse, workspace=None, stream=None):
+    """``mstar_attn_fwd`` on torch tensors."""
+    dev = _check_fwd_tensors(pl, q, k_pages, v_pages, block_table, out, lse)
     need = pl.workspace_bytes
     ws_ptr, ws_bytes = None, 0
     if workspace is not None:
@@ -383,6 +393,15 @@ def fwd(pl: Plan, q, k_pages, v_pages, block_table, out, lse, workspace=None, st
     _check_rc(lib().mstar_attn_fwd(pl.handle, q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
                                    block_table.data_ptr(), out.data_ptr(), lse.data_ptr(), ws_ptr, ws_bytes,
                                    _stream_handle(stream)))
+
+
+def fwd_noalloc(pl: Plan, q, k_pages, v_pages, block_table, out, lse, stream=None):
+    """``mstar_attn_fwd_noalloc`` on torch tensors: split-K partials in the
+    library's static device scratch instead of a workspace."""
+    _check_fwd_tensors(pl, q, k_pages, v_pages, block_table, out, lse)
+    _check_rc(lib().mstar_attn_fwd_noalloc(pl.handle, q.data_ptr(), k_pages.data_ptr(), v_pages.data_ptr(),
+                                           block_table.data_ptr(), out.data_ptr(), lse.data_ptr(),
+                                           _stream_handle(stream)))
 
 
 def kv_append(pl: Plan, k_new, v_new, block_table, k_pages, v_pages, stream=None):

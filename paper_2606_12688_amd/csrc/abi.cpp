@@ -432,6 +432,26 @@ MSTAR_EXPORT int mstar_attn_fwd_timed(const mstar_plan_t* plan, const void* q, c
     return MSTAR_OK;
 }
 
+MSTAR_EXPORT int mstar_attn_fwd_noalloc(const mstar_plan_t* plan, const void* q, const void* k_pages,
+                                        const void* v_pages, const int32_t* block_table, void* out, float* lse,
+                                        hipStream_t stream) {
+    if (!plan) return fail(MSTAR_ERR_INVALID_ARG, "plan is NULL");
+    const size_t need = mstar_attn_workspace_bytes(plan);
+    if (need > mstar::kScratchBytes)
+        return fail(MSTAR_ERR_WORKSPACE, "the plan needs " + std::to_string(need) +
+                                             " bytes of scratch, more than the " +
+                                             std::to_string(mstar::kScratchBytes) +
+                                             " the allocation-free entry point holds; use mstar_attn_fwd");
+    if (!plan->dev) return fail(MSTAR_ERR_INVALID_ARG, "plan was built host-only");
+    void* ws = nullptr;
+    if (need > 0) {
+        hipError_t e = mstar::scratch_buffer(&ws);
+        if (e != hipSuccess) return hip_fail(e, "scratch address");
+    }
+    return mstar_attn_fwd_timed(plan, q, k_pages, v_pages, block_table, out, lse, ws, need > 0 ? mstar::kScratchBytes : 0,
+                                stream, nullptr, nullptr);
+}
+
 MSTAR_EXPORT int mstar_kv_append(const mstar_plan_t* plan, const void* k_new, const void* v_new,
                                  const int32_t* block_table, void* k_pages, void* v_pages, hipStream_t stream) {
     if (!plan) return fail(MSTAR_ERR_INVALID_ARG, "plan is NULL");

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "mstar_attn.h"
 #include "plan_types.h"
 
 namespace mstar {
@@ -59,5 +60,10 @@ hipError_t launch_append(const AArgs& a, hipStream_t s);
 hipError_t launch_few(const KArgs& a, int head_dim, int row_blocks, hipStream_t s);
 hipError_t launch_f32(const KArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_merge(const MArgs& a, int head_dim, bool bf16_out, hipStream_t s);
+
+// Device scratch for the allocation-free entry point (a static device array of
+// kScratchBytes per GPU): its device address on the current device.
+constexpr size_t kScratchBytes = MSTAR_NOALLOC_SCRATCH_BYTES;
+hipError_t scratch_buffer(void** ptr);
 
 }  // namespace mstar

@@ -18,7 +18,16 @@
 // and lse = (m2 + log2 l) * ln 2 at the end.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "kernels.h"
+
+// Device scratch of the allocation-free entry point: the split-K partials of
+// one call (fp32 partial rows, then their log-sum-exps) live here instead of
+// in a caller workspace.  One copy per GPU, held until the process ends.  In
+// host code this name is a host-side stand-in, never a device address: the
+// device address comes from hipGetSymbolAddress (scratch_buffer below).
+static __device__ __align__(256) unsigned char scratch[mstar::kScratchBytes];
 
 namespace mstar {
 namespace {
@@ -1223,6 +1232,29 @@ hipError_t launch_f32(const KArgs& a, int head_dim, hipStream_t s) {
     else
         hipLaunchKernelGGL(f32_kernel<128>, dim3(a.n_items), dim3(256), 0, s, a);
     return hipGetLastError();
+}
+
+hipError_t scratch_buffer(void** ptr) {
+    // the array's device address, looked up once per device with that device
+    // current (each GPU holds its own copy at its own address)
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    *ptr = nullptr;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_merge(const MArgs& a, int head_dim, bool bf16_out, hipStream_t s) {

@@ -11,4 +11,8 @@ hipError_t launch_append(const AArgs&, hipStream_t) { return hipErrorNotSupporte
 hipError_t launch_few(const KArgs&, int, int, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_f32(const KArgs&, int, hipStream_t) { return hipErrorNotSupported; }
 hipError_t launch_merge(const MArgs&, int, bool, hipStream_t) { return hipErrorNotSupported; }
+hipError_t scratch_buffer(void** ptr) {
+    *ptr = nullptr;
+    return hipErrorNotSupported;
+}
 }  // namespace mstar

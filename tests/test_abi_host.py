@@ -425,3 +425,22 @@ def test_near_equal_units_that_fill_the_gpu_stay_whole():
     pl = plan_for(b, attn.FLAG_HOST_ONLY)
     assert pl.stats()["merge_rows"] > 0
     pl.destroy()
+
+
+def test_noalloc_entry_point_refuses_plans_beyond_its_scratch_on_the_host():
+    """The size check of mstar_attn_fwd_noalloc happens on the host before
+    anything else: a host-only plan needing more than the static scratch is
+    refused with MSTAR_ERR_WORKSPACE (nothing is dereferenced), one within it
+    reaches the usual host-only refusal."""
+    b = W.FULL_SIZE["decode_bf16"]()
+    L = attn.lib()
+    pl = plan_for(b, attn.FLAG_FORCE_SPLIT | attn.FLAG_HOST_ONLY)
+    assert pl.workspace_bytes > 32 << 20
+    assert L.mstar_attn_fwd_noalloc(pl.handle, 16, 16, 16, 16, 16, 16, None) == attn.ERR_WORKSPACE
+    assert "scratch" in attn.last_error()
+    pl.destroy()
+    pl = plan_for(b, attn.FLAG_HOST_ONLY)
+    assert 0 < pl.workspace_bytes <= 32 << 20
+    assert L.mstar_attn_fwd_noalloc(pl.handle, 16, 16, 16, 16, 16, 16, None) == attn.ERR_INVALID_ARG
+    assert "host-only" in attn.last_error()
+    pl.destroy()
