@@ -220,6 +220,25 @@ __device__ __forceinline__ bool softmax_update(const RowGroup& rg, f32x4 (&s)[RB
     return rescale;
 }
 
+// Probabilities against a fixed per-row reference m: p = 2^(c s - m), with no
+// maximum; hidden keys are -inf and give 0.  ts receives the lane's partial
+// sums of the tile.
+template <int RB, int NB>
+__device__ __forceinline__ void softmax_fixed(f32x4 (&s)[RB][NB], float c, const float (&m)[RB], float (&ts)[RB]) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) s[rb][kb][i] = fast_exp2(fmaf(s[rb][kb][i], c, -m[rb]));
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) ts[rb] = tree_sum<NB>(s[rb]);
+}
+// Bound on a lane's partial sum of one tile under the fixed reference: below
+// it every probability is below 2^32, far from overflow of the sums and the
+// weighted values; at or above it (or inf / NaN) the tile is redone exactly.
+constexpr float kFixedTileLimit = 4294967296.0f;  // 2^32
+
 // ---------------------------------------------------------------------------
 // Multi-row tile kernel: one workgroup = 64 * RBW query rows of one query head
 // (4 waves x RBW blocks of 16 rows) against the item's key range, 64 keys per
@@ -327,6 +346,9 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
     __shared__ __attribute__((aligned(1024))) char buf0[2][TB];  // [K, V] of even tiles
     __shared__ __attribute__((aligned(1024))) char buf1[2][TB];  // [K, V] of odd tiles
     __shared__ __attribute__((aligned(256))) int32_t page_ring[2][64];
+    // each row's visible interval [lo, hi), read on partial tiles only (kept
+    // out of the registers the tile loop carries)
+    __shared__ __attribute__((aligned(16))) int2 row_lohi[4][16 * RBW];
 
     // The planner's launch order names the (item, query head) of every
     // workgroup; it keeps the workgroups that read the same K/V pages on one
@@ -347,7 +369,7 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
     // CASC (a shared-prefix cascade item): row r is entry row0 + r of the row
     // list, a (packed query row, query head) of some group member; every key
     // of the item is visible to it.
-    int32_t lo[RBW], hi[RBW];
+    int32_t lo[RBW], hi[RBW];  // written to row_lohi, read back on partial tiles
     bool valid[RBW];
     bf16x8 qf[RBW][DS];
 #pragma unroll
@@ -375,6 +397,10 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
             }
         }
     }
+    if (grp == 0) {
+#pragma unroll
+        for (int rb = 0; rb < RBW; ++rb) row_lohi[wave][rb * 16 + n] = make_int2(lo[rb], hi[rb]);
+    }
     // wave-uniform bounds: intervals never shrink from one row to the next
     const int wr0 = wave * 16 * RBW;
     const int wr1 = min(wr0 + 16 * RBW - 1, it.nrows - 1);
@@ -395,9 +421,11 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
     for (int rb = 0; rb < RBW; ++rb)
 #pragma unroll
         for (int db = 0; db < DB; ++db) o[rb][db] = f32x4{0, 0, 0, 0};
+    // Rows past the item's end (never stored) start with reference 0, so that
+    // the fixed mode below never meets an infinite reference.
 #pragma unroll
     for (int rb = 0; rb < RBW; ++rb) {
-        m[rb] = kNegInf;
+        m[rb] = valid[rb] ? kNegInf : 0.0f;
         l[rb] = 0.0f;
     }
 
@@ -517,16 +545,7 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
 
     // ---- one tile: scores, mask, online softmax, weighted values ---------------
     const float c2 = a.scale_log2;
-    auto compute_tile = [&](int tix, const char (&cur)[2][TB]) {
-        const int32_t k0 = it.k_begin + tix * BN;
-        if (!(wave_active && k0 < w_hi_max && k0 + BN > w_lo_min)) return;
-        // the compiler's interleaving strategy for LDS reads among MFMAs
-        // (1-2% at d = 128, neutral at d = 64)
-        __builtin_amdgcn_iglp_opt(0);
-        const char* kl = &cur[0][0];
-        const char* vl = &cur[1][0];
-        const bool full = k0 >= w_lo_max && k0 + BN <= w_hi_min;
-        f32x4 sc[RBW][4];
+    auto scores = [&](const char* kl, f32x4 (&sc)[RBW][4]) {
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
             bf16x8 kf[DS];
@@ -539,32 +558,32 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
 #pragma unroll
                 for (int rb = 0; rb < RBW; ++rb) sc[rb][kb] = mfma16(kf[s], qf[rb][s], sc[rb][kb]);
         }
-        if (!full) {
+    };
+    auto mask = [&](int32_t k0, f32x4 (&sc)[RBW][4]) {
 #pragma unroll
-            for (int rb = 0; rb < RBW; ++rb) {
-                // key k0 + 4 grp + c is visible iff lo <= key < hi
-                const int32_t lo_r = lo[rb] - (k0 + 4 * grp), hi_r = hi[rb] - (k0 + 4 * grp);
+        for (int rb = 0; rb < RBW; ++rb) {
+            // key k0 + 4 grp + c is visible iff lo <= key < hi
+            const int2 lh = row_lohi[wave][rb * 16 + n];
+            const int32_t lo_r = lh.x - (k0 + 4 * grp), hi_r = lh.y - (k0 + 4 * grp);
 #pragma unroll
-                for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int c = kb * 16 + i;
-                        if (!(c >= lo_r && c < hi_r)) sc[rb][kb][i] = kNegInf;
-                    }
-            }
+                for (int i = 0; i < 4; ++i) {
+                    const int c = kb * 16 + i;
+                    if (!(c >= lo_r && c < hi_r)) sc[rb][kb][i] = kNegInf;
+                }
         }
-        float alpha[RBW];
-        if (softmax_update<RBW, 4>(rg, sc, c2, m, l, alpha)) {
+    };
+    // probabilities as the bf16 B operands of the value product (32-key halves)
+    auto pack = [&](const f32x4 (&sc)[RBW][4], bf16x8 (&pf)[2][RBW]) {
 #pragma unroll
-            for (int rb = 0; rb < RBW; ++rb)
+        for (int c = 0; c < 2; ++c)
 #pragma unroll
-                for (int db = 0; db < DB; ++db) o[rb][db] *= alpha[rb];
-        }
+            for (int rb = 0; rb < RBW; ++rb) pf[c][rb] = to_bf16x8(sc[rb][2 * c], sc[rb][2 * c + 1]);
+    };
+    auto values = [&](const char* vl, const bf16x8 (&pf)[2][RBW]) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
-            bf16x8 pf[RBW];
-#pragma unroll
-            for (int rb = 0; rb < RBW; ++rb) pf[rb] = to_bf16x8(sc[rb][2 * c], sc[rb][2 * c + 1]);
             bf16x8 vf[DB];
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
@@ -574,8 +593,74 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
 #pragma unroll
             for (int db = 0; db < DB; ++db)
 #pragma unroll
-                for (int rb = 0; rb < RBW; ++rb) o[rb][db] = mfma16(vf[db], pf[rb], o[rb][db]);
+                for (int rb = 0; rb < RBW; ++rb) o[rb][db] = mfma16(vf[db], pf[c][rb], o[rb][db]);
         }
+    };
+    // Two softmax modes.  Exact: the tile's row maxima are taken and the
+    // reference moved lazily (softmax_update); used on a wave's tiles until
+    // every valid row of the wave has a reference.  Fixed: probabilities
+    // against each row's reference as it stands, with no maximum at all (an
+    // fma, an exp2 and a sum per score), which takes the reductions and the
+    // cross-lane exchange out of the tile.  Both are exact (out = O / l and
+    // lse = m + log2 l share the reference).  A fixed-mode tile whose sums
+    // reach kFixedTileLimit (scores far above the reference) is redone in exact
+    // mode from its scores, recomputed from the K tile still in LDS.
+    bool need_ref = true;  // wave-uniform: some valid row of the wave has no reference yet
+    auto exact_update = [&](f32x4 (&sc)[RBW][4]) {
+        float alpha[RBW];
+        if (softmax_update<RBW, 4>(rg, sc, c2, m, l, alpha)) {
+#pragma unroll
+            for (int rb = 0; rb < RBW; ++rb)
+#pragma unroll
+                for (int db = 0; db < DB; ++db) o[rb][db] *= alpha[rb];
+        }
+    };
+    auto compute_tile = [&](int tix, const char (&cur)[2][TB]) {
+        const int32_t k0 = it.k_begin + tix * BN;
+        if (!(wave_active && k0 < w_hi_max && k0 + BN > w_lo_min)) return;
+        // the compiler's interleaving strategy for LDS reads among MFMAs
+        // (1-2% at d = 128, neutral at d = 64)
+        __builtin_amdgcn_iglp_opt(0);
+        const char* kl = &cur[0][0];
+        const char* vl = &cur[1][0];
+        const bool full = k0 >= w_lo_max && k0 + BN <= w_hi_min;
+        f32x4 sc[RBW][4];
+        bf16x8 pf[2][RBW];
+        scores(kl, sc);
+        if (!full) mask(k0, sc);
+        bool exact = need_ref;
+        if (!need_ref) {
+            float ts[RBW];
+            softmax_fixed<RBW, 4>(sc, c2, m, ts);
+            bool over = false;
+#pragma unroll
+            for (int rb = 0; rb < RBW; ++rb) over |= !(ts[rb] < kFixedTileLimit);
+            exact = __builtin_amdgcn_ballot_w64(over) != 0;
+            if (!exact) {
+#pragma unroll
+                for (int rb = 0; rb < RBW; ++rb) l[rb] += ts[rb];
+                pack(sc, pf);
+            }
+        }
+        if (exact) {
+            if (!need_ref) {
+                // a fixed-mode tile out of range: its scores again, from an
+                // opaque copy of the K tile's address so that the compiler
+                // loads the fragments anew instead of keeping the first ones
+                // (and the raw scores) alive through the softmax
+                uint32_t ka = lds_address(kl);
+                asm volatile("" : "+s"(ka));
+                scores((const char*)((const lds_char*)(uintptr_t)ka), sc);
+                if (!full) mask(k0, sc);
+            }
+            exact_update(sc);
+            bool missing = false;
+#pragma unroll
+            for (int rb = 0; rb < RBW; ++rb) missing |= m[rb] == kNegInf;
+            need_ref = __builtin_amdgcn_ballot_w64(missing) != 0;
+            pack(sc, pf);
+        }
+        values(vl, pf);
     };
 
     const int n_tiles = (it.k_end - it.k_begin + BN - 1) / BN;
