@@ -498,21 +498,28 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
         // first tile of window w >= 1: every wave is past its last read of
         // window w - 1, so its ring slot can take window w + 1
         if (tix > 0 && (rel0 & 63) == 0) load_window((rel0 >> 6) + 1);
-        // the tile's PPT page indices, one 16-byte LDS read
-        const int4 pq = *reinterpret_cast<const int4*>(&page_ring[(rel0 >> 6) & 1][rel0 & 63]);
-        const int32_t pgs[4] = {pq.x, pq.y, pq.z, pq.w};
+        // page of load j within the tile: (4 j + wave) RPL / 16.  With RPL = 4
+        // (d = 128) it is j for every wave: one 16-byte LDS read holds the
+        // tile's four.  Otherwise each wave reads its own indices at a
+        // wave-uniform LDS address, with no per-lane selection.
+        const int32_t* ring = &page_ring[(rel0 >> 6) & 1][rel0 & 63];
         uint32_t page[NLD];
+        if constexpr (RPL == 4) {
+            const int4 pq = *reinterpret_cast<const int4*>(ring);
+            const int32_t pgs[4] = {pq.x, pq.y, pq.z, pq.w};
+#pragma unroll
+            for (int j = 0; j < NLD; ++j) page[j] = (uint32_t)__builtin_amdgcn_readfirstlane(pgs[j]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < NLD; ++j)
+                page[j] = (uint32_t)__builtin_amdgcn_readfirstlane(ring[((4 * j + wave) * RPL) >> 4]);
+        }
         bool all_ok = true;
 #pragma unroll
-        for (int j = 0; j < NLD; ++j) {
-            // page of load j within the tile: (4 j + wave) RPL / 16, split so
-            // that the compiler sees a constant for RPL = 4
-            page[j] = (uint32_t)__builtin_amdgcn_readfirstlane(pgs[(j * RPL) / 4 + (wave * RPL) / 16]);
-            all_ok &= page[j] < (uint32_t)a.num_pages;
-        }
+        for (int j = 0; j < NLD; ++j) all_ok &= page[j] < (uint32_t)a.num_pages;
         const int32_t k0 = it.k_begin + tix * BN;
         const bool tail = k0 + BN > it.k_end;
-        if (SMALL && all_ok && !tail) {
+        if (__builtin_expect(SMALL && all_ok && !tail, 1)) {
             // common case: only the page offsets change from tile to tile
 #pragma unroll
             for (int j = 0; j < NLD; ++j) {

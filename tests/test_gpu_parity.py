@@ -234,6 +234,7 @@ def test_full_size_sampled(name, cascade):
 @pytest.mark.parametrize("name,rate,cascade", [("decode_bf16", 0.03, False), ("text_latent_bf16", 0.03, False),
                                                ("stream_window_bf16", 0.03, False), ("rollout_bf16", 0.05, False),
                                                ("decode_bf16", -0.0006, False),
+                                               ("rollout_bf16", 0.5, False), ("text_latent_bf16", 0.5, False),
                                                ("shared_prefix_decode_bf16", 0.03, True),
                                                ("rollout_bf16", 0.05, True)])
 def test_growing_scores_move_the_lazy_reference(name, rate, cascade, flag):
@@ -241,7 +242,10 @@ def test_growing_scores_move_the_lazy_reference(name, rate, cascade, flag):
     growing from tile to tile, by about the lazy threshold of 2^8 per 64-key
     tile, so the kernels both keep a stale reference (probabilities up to 2^8)
     and move it (rescaling O); split pieces then carry very different LSEs
-    into the merge.  With rate < 0 the maximum sits in the first keys.
+    into the merge.  With rate < 0 the maximum sits in the first keys.  With
+    rate 0.5 the scores of later tiles overflow fp32 against the reference of
+    a row's first tile (2^100 and beyond), so the tile kernel's fixed-reference
+    tiles must be redone in exact mode.
 
     Peaked rows return single V values of magnitude up to ~4.5, where storing
     the output in bf16 alone can be off by half a unit in the last place,
