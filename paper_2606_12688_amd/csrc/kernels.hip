@@ -111,6 +111,15 @@ __device__ __forceinline__ uint4 load16_at(__amdgpu_buffer_rsrc_t r, uint32_t by
 __device__ __forceinline__ uint4 load16(const void* base, int64_t elem_off_bf16) {
     return *reinterpret_cast<const uint4*>(reinterpret_cast<const bf16_t*>(base) + elem_off_bf16);
 }
+// The same with the non-temporal hint: for data read once (a tile's Q rows),
+// so that it does not push shared K/V lines out of the caches (text+latent
+// launch: fetched bytes 527 -> 334 MB, of which 250 MB are Q).
+__device__ __forceinline__ uint4 load16_nt(const void* base, int64_t elem_off_bf16) {
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 w =
+        __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(reinterpret_cast<const bf16_t*>(base) + elem_off_bf16));
+    return __builtin_bit_cast(uint4, w);
+}
 
 // Visible interval of query row i of a request, clipped to the item's keys.
 __device__ __forceinline__ void row_interval(const KArgs& a, const SeqInfo& si, const WorkItem& it,
@@ -390,7 +399,7 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
 #pragma unroll
         for (int s = 0; s < DS; ++s) {
             if (valid[rb]) {
-                uint4 u = load16(a.q, qoff + 32 * s + 8 * grp);
+                uint4 u = load16_nt(a.q, qoff + 32 * s + 8 * grp);
                 qf[rb][s] = __builtin_bit_cast(bf16x8, u);
             } else {
                 qf[rb][s] = bf16x8{};
