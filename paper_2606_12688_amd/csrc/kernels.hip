@@ -335,17 +335,31 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
 // valid offset in range and pushes the marker offset below out of range.
 constexpr uint32_t kSmallPoolBytes = 0x80000000u;
 
-// Occupancy: two workgroups per CU at d = 128 (64 KB of LDS and up to 256
-// VGPRs each), four at d = 64 (32 KB, at most 128 VGPRs: the softmax's vector
-// work, which bounds d = 64, then has four waves per SIMD to draw from).
-template <int D, int RBW, bool SMALL, bool CASC>
-__global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
-    constexpr int BN = kTileKeys;
+// Keys per tile of the d = 128 tile kernel: 32-key tiles (32 KB of LDS, 162
+// VGPRs) run three workgroups per CU instead of two with 64-key tiles, which
+// the extra barrier per 32 keys more than pays for (text+latent 1.788 ->
+// 1.713 ms, CFG labels 2.120 -> 2.006 ms).  At d = 64 the 64-key tile stays:
+// 32-key tiles at five workgroups per CU were 1.6% slower.
+#ifndef MSTAR_TILE_KEYS_D128
+#define MSTAR_TILE_KEYS_D128 32
+#endif
+constexpr int kTileKeysD128 = MSTAR_TILE_KEYS_D128;
+
+// Occupancy: two workgroups per CU at d = 128 with 64-key tiles (64 KB of
+// LDS and up to 256 VGPRs each), four at d = 64 (32 KB, at most 128 VGPRs: the
+// softmax's vector work, which bounds d = 64, then has four waves per SIMD to
+// draw from).  BN keys per tile: 64, or 32 (half the LDS and score registers
+// for a third workgroup per CU at d = 128, with a barrier per 32 keys).
+template <int D, int RBW, bool SMALL, bool CASC, int BN>
+__global__ __launch_bounds__(256, D == 64 ? 4 : (BN == 32 ? 3 : 2)) void tile_kernel(KArgs a) {
+    static_assert(BN == 32 || BN == 64, "tile sizes");
+    constexpr int NB = BN / 16;      // 16-key blocks of a tile
+    constexpr int NC = BN / 32;      // 32-key steps of the value product
     constexpr int RBY = 2 * D;       // bytes per K/V row in LDS
     constexpr int CH = D / 8;        // 16-byte chunks per row
     constexpr int DS = D / 32;       // MFMA steps over the head dimension
     constexpr int DB = D / 16;       // 16-wide blocks of O^T
-    constexpr int NLD = CH / 4;      // direct loads per wave, matrix and tile
+    constexpr int NLD = BN * CH / 256;  // direct loads per wave, matrix and tile
     constexpr int RPL = 64 / CH;     // rows filled by one wave-wide load
     constexpr int TB = BN * RBY;     // bytes of one K or V tile
     constexpr int PPT = BN / 16;     // pages per tile
@@ -513,11 +527,15 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
         // wave-uniform LDS address, with no per-lane selection.
         const int32_t* ring = &page_ring[(rel0 >> 6) & 1][rel0 & 63];
         uint32_t page[NLD];
-        if constexpr (RPL == 4) {
+        if constexpr (RPL == 4 && NLD == 4) {
             const int4 pq = *reinterpret_cast<const int4*>(ring);
             const int32_t pgs[4] = {pq.x, pq.y, pq.z, pq.w};
 #pragma unroll
             for (int j = 0; j < NLD; ++j) page[j] = (uint32_t)__builtin_amdgcn_readfirstlane(pgs[j]);
+        } else if constexpr (RPL == 4) {
+            const int2 pq = *reinterpret_cast<const int2*>(ring);
+            page[0] = (uint32_t)__builtin_amdgcn_readfirstlane(pq.x);
+            page[1] = (uint32_t)__builtin_amdgcn_readfirstlane(pq.y);
         } else {
 #pragma unroll
             for (int j = 0; j < NLD; ++j)
@@ -561,9 +579,9 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
 
     // ---- one tile: scores, mask, online softmax, weighted values ---------------
     const float c2 = a.scale_log2;
-    auto scores = [&](const char* kl, f32x4 (&sc)[RBW][4]) {
+    auto scores = [&](const char* kl, f32x4 (&sc)[RBW][NB]) {
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
+        for (int kb = 0; kb < NB; ++kb) {
             bf16x8 kf[DS];
 #pragma unroll
             for (int s = 0; s < DS; ++s) kf[s] = *reinterpret_cast<const bf16x8*>(kl + kb * 16 * RBY + koff[s]);
@@ -575,14 +593,14 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
                 for (int rb = 0; rb < RBW; ++rb) sc[rb][kb] = mfma16(kf[s], qf[rb][s], sc[rb][kb]);
         }
     };
-    auto mask = [&](int32_t k0, f32x4 (&sc)[RBW][4]) {
+    auto mask = [&](int32_t k0, f32x4 (&sc)[RBW][NB]) {
 #pragma unroll
         for (int rb = 0; rb < RBW; ++rb) {
             // key k0 + 4 grp + c is visible iff lo <= key < hi
             const int2 lh = row_lohi[wave][rb * 16 + n];
             const int32_t lo_r = lh.x - (k0 + 4 * grp), hi_r = lh.y - (k0 + 4 * grp);
 #pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
+            for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int c = kb * 16 + i;
@@ -591,15 +609,15 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
         }
     };
     // probabilities as the bf16 B operands of the value product (32-key halves)
-    auto pack = [&](const f32x4 (&sc)[RBW][4], bf16x8 (&pf)[2][RBW]) {
+    auto pack = [&](const f32x4 (&sc)[RBW][NB], bf16x8 (&pf)[NC][RBW]) {
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
+        for (int c = 0; c < NC; ++c)
 #pragma unroll
             for (int rb = 0; rb < RBW; ++rb) pf[c][rb] = to_bf16x8(sc[rb][2 * c], sc[rb][2 * c + 1]);
     };
-    auto values = [&](const char* vl, const bf16x8 (&pf)[2][RBW]) {
+    auto values = [&](const char* vl, const bf16x8 (&pf)[NC][RBW]) {
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
+        for (int c = 0; c < NC; ++c) {
             bf16x8 vf[DB];
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
@@ -622,9 +640,9 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
     // reach kFixedTileLimit (scores far above the reference) is redone in exact
     // mode from its scores, recomputed from the K tile still in LDS.
     bool need_ref = true;  // wave-uniform: some valid row of the wave has no reference yet
-    auto exact_update = [&](f32x4 (&sc)[RBW][4]) {
+    auto exact_update = [&](f32x4 (&sc)[RBW][NB]) {
         float alpha[RBW];
-        if (softmax_update<RBW, 4>(rg, sc, c2, m, l, alpha)) {
+        if (softmax_update<RBW, NB>(rg, sc, c2, m, l, alpha)) {
 #pragma unroll
             for (int rb = 0; rb < RBW; ++rb)
 #pragma unroll
@@ -640,14 +658,14 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : 2) void tile_kernel(KArgs a) {
         const char* kl = &cur[0][0];
         const char* vl = &cur[1][0];
         const bool full = k0 >= w_lo_max && k0 + BN <= w_hi_min;
-        f32x4 sc[RBW][4];
-        bf16x8 pf[2][RBW];
+        f32x4 sc[RBW][NB];
+        bf16x8 pf[NC][RBW];
         scores(kl, sc);
         if (!full) mask(k0, sc);
         bool exact = need_ref;
         if (!need_ref) {
             float ts[RBW];
-            softmax_fixed<RBW, 4>(sc, c2, m, ts);
+            softmax_fixed<RBW, NB>(sc, c2, m, ts);
             bool over = false;
 #pragma unroll
             for (int rb = 0; rb < RBW; ++rb) over |= !(ts[rb] < kFixedTileLimit);
@@ -1288,11 +1306,11 @@ hipError_t launch_tiles(const KArgs& a, int head_dim, hipStream_t s) {
     const uint64_t pool_bytes = (uint64_t)a.num_pages * 16 * a.hkv * head_dim * 2;
     const bool small = pool_bytes <= kSmallPoolBytes;
     if (head_dim == 64) {
-        if (small) hipLaunchKernelGGL((tile_kernel<64, 2, true, false>), g, b, 0, s, a);
-        else hipLaunchKernelGGL((tile_kernel<64, 2, false, false>), g, b, 0, s, a);
+        if (small) hipLaunchKernelGGL((tile_kernel<64, 2, true, false, 64>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((tile_kernel<64, 2, false, false, 64>), g, b, 0, s, a);
     } else {
-        if (small) hipLaunchKernelGGL((tile_kernel<128, 2, true, false>), g, b, 0, s, a);
-        else hipLaunchKernelGGL((tile_kernel<128, 2, false, false>), g, b, 0, s, a);
+        if (small) hipLaunchKernelGGL((tile_kernel<128, 2, true, false, kTileKeysD128>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((tile_kernel<128, 2, false, false, kTileKeysD128>), g, b, 0, s, a);
     }
     return hipGetLastError();
 }
@@ -1303,11 +1321,11 @@ hipError_t launch_cascade(const KArgs& a, int head_dim, hipStream_t s) {
     const uint64_t pool_bytes = (uint64_t)a.num_pages * 16 * a.hkv * head_dim * 2;
     const bool small = pool_bytes <= kSmallPoolBytes;
     if (head_dim == 64) {
-        if (small) hipLaunchKernelGGL((tile_kernel<64, 2, true, true>), g, b, 0, s, a);
-        else hipLaunchKernelGGL((tile_kernel<64, 2, false, true>), g, b, 0, s, a);
+        if (small) hipLaunchKernelGGL((tile_kernel<64, 2, true, true, 64>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((tile_kernel<64, 2, false, true, 64>), g, b, 0, s, a);
     } else {
-        if (small) hipLaunchKernelGGL((tile_kernel<128, 2, true, true>), g, b, 0, s, a);
-        else hipLaunchKernelGGL((tile_kernel<128, 2, false, true>), g, b, 0, s, a);
+        if (small) hipLaunchKernelGGL((tile_kernel<128, 2, true, true, kTileKeysD128>), g, b, 0, s, a);
+        else hipLaunchKernelGGL((tile_kernel<128, 2, false, true, kTileKeysD128>), g, b, 0, s, a);
     }
     return hipGetLastError();
 }
