@@ -374,11 +374,12 @@ int mstar_kv_append(const mstar_plan_t* plan, const void* k_new, const void* v_n
 
 /* Release the plan: its host memory is freed and its device buffers, staging
  * copy, events and side stream go back to the per-device pool (no HIP call,
- * no device synchronization).  Work that fwd or kv_append enqueued outside
- * graph capture may still be running: a later plan that takes the same
- * buffers waits for it on the device before overwriting them.  A graph that
- * captured the plan's calls must not be replayed after the plan is
- * destroyed.  NULL is ignored. */
+ * no device synchronization).  The work of the plan's last fwd or kv_append
+ * call enqueued outside graph capture may still be running: a later plan that
+ * takes the same buffers waits for it on the device before overwriting them.
+ * Calls with the plan on other streams than the last one must have completed
+ * (the caller orders them), and a graph that captured the plan's calls must
+ * not be replayed after the plan is destroyed.  NULL is ignored. */
 void mstar_attn_plan_destroy(mstar_plan_t* plan);
 
 /* Message for the calling thread's last failing call ("" if none). */

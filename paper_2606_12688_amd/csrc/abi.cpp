@@ -225,7 +225,11 @@ static int plan_impl(const mstar_attn_params* params, const mstar_seq_desc* seqs
         }
         plan->blk = b;
         plan->dev = b->dev;
+        // a failure after the upload was enqueued: let that copy finish
+        // (best effort) before the block goes back to the pool
+        bool enqueued = false;
         auto give_up = [&](hipError_t err, const char* what) {
+            if (enqueued) (void)hipStreamSynchronize(up);
             release_block(b);
             delete plan;
             return hip_fail(err, what);
@@ -251,6 +255,7 @@ static int plan_impl(const mstar_attn_params* params, const mstar_seq_desc* seqs
         // must be done before the upload overwrites it (a device-side wait)
         if (b->last_use_set && (e = hipStreamWaitEvent(up, b->last_use, 0)) != hipSuccess)
             return give_up(e, "hipStreamWaitEvent(plan reuse)");
+        enqueued = true;
         if ((e = hipMemcpyAsync(b->dev, b->pinned, plan->bytes, hipMemcpyHostToDevice, up)) != hipSuccess)
             return give_up(e, "plan upload");
         if ((e = hipEventRecord(b->uploaded, up)) != hipSuccess) return give_up(e, "hipEventRecord(plan upload)");
