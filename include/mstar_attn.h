@@ -141,6 +141,7 @@ typedef struct {
     int64_t partial_slots;   /* fp32 partial rows in the workspace                          */
     int64_t total_q;         /* packed query rows (max q_start + q_len)                     */
     double plan_host_us;     /* host time spent building the plan                           */
+    int64_t device_bytes;    /* bytes of the work list's device copy (host-only: would-be)   */
 } mstar_plan_stats;
 
 /* ---- entry points -------------------------------------------------------- */
@@ -158,7 +159,8 @@ typedef struct {
  * before fwd (same stream, or synchronize).  The work list's device buffer,
  * its pinned staging copy and (for a plan whose fwd runs the few-row kernel
  * beside the tile kernel) a side stream come from a per-device pool that
- * destroyed plans return them to: only the first plans of a process, or a
+ * destroyed plans return them to (the smallest free buffer that fits, the
+ * most recently returned among equals): only the first plans of a process, or a
  * plan larger than every pooled buffer, allocate (hipMalloc, hipHostMalloc,
  * hipStreamCreate); steady-state planning allocates no device memory and
  * makes no device-synchronizing call.  A pooled buffer's upload first waits,

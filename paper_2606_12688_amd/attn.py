@@ -90,7 +90,8 @@ class PlanStats(ctypes.Structure):
     _fields_ = [("visible_pairs", ctypes.c_int64), ("prefill_items", ctypes.c_int64),
                 ("decode_items", ctypes.c_int64), ("f32_items", ctypes.c_int64),
                 ("merge_rows", ctypes.c_int64), ("partial_slots", ctypes.c_int64),
-                ("total_q", ctypes.c_int64), ("plan_host_us", ctypes.c_double)]
+                ("total_q", ctypes.c_int64), ("plan_host_us", ctypes.c_double),
+                ("device_bytes", ctypes.c_int64)]
 
 
 class MStarError(RuntimeError):

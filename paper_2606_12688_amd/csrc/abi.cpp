@@ -65,7 +65,8 @@ void free_block(PlanBlock* b) {
 }
 
 // A block of at least `bytes` on the current device: the smallest fitting free
-// one, else a new one (capacity rounded up to a power of two).
+// one, the most recently released among equals (its staging copy is the most
+// likely to be cache-warm), else a new one (capacity rounded up to a power of two).
 hipError_t acquire_block(size_t bytes, PlanBlock** out) {
     *out = nullptr;
     int dev = 0;
@@ -74,7 +75,7 @@ hipError_t acquire_block(size_t bytes, PlanBlock** out) {
     {
         std::lock_guard<std::mutex> lk(g_pool_mu);
         size_t best = g_pool.size();
-        for (size_t i = 0; i < g_pool.size(); ++i)
+        for (size_t i = g_pool.size(); i-- > 0;)
             if (g_pool[i]->device == dev && g_pool[i]->bytes >= bytes &&
                 (best == g_pool.size() || g_pool[i]->bytes < g_pool[best]->bytes))
                 best = i;
@@ -522,6 +523,7 @@ MSTAR_EXPORT int mstar_attn_plan_stats(const mstar_plan_t* plan, mstar_plan_stat
     out->partial_slots = h.partial_slots;
     out->total_q = h.total_q;
     out->plan_host_us = plan->plan_us;
+    out->device_bytes = (int64_t)plan->bytes;
     return MSTAR_OK;
 }
 

@@ -119,6 +119,9 @@ def test_full_size_plans(name):
     else:
         assert st["prefill_items"] == 0 and st["decode_items"] > 0
     assert st["plan_host_us"] < 5e5
+    # the work list: request records, per-row bounds and the 32-byte items, each section 256-aligned
+    assert st["device_bytes"] % 256 == 0
+    assert st["device_bytes"] >= 4 * st["total_q"] + 32 * (st["prefill_items"] + st["decode_items"] + st["f32_items"])
     pl.destroy()
 
 
