@@ -307,9 +307,8 @@ __device__ __forceinline__ void wait_vmem() {
 
 // 16-byte direct global -> LDS load of one wave through the compiler's
 // builtin (lane i writes bytes [16 i, 16 i + 16) after `lds`, which must be
-// wave-uniform).  The compiler tracks it: it waits for it before a read of
-// the same LDS array, so buffers that must not be waited for together live
-// in distinct arrays.  The load is marked non-temporal (the NT cache-policy bit): the few-row
+// wave-uniform).  The compiler tracks it and waits for it before later LDS
+// reads.  The load is marked non-temporal (the NT cache-policy bit): the few-row
 // kernel reads each V row of a request once, so its lines go first when the
 // caches need room (decode batch: 0.617 -> 0.676 of HBM peak; 16-token
 // chunks: 0.593 -> 0.618).  Marking the K loads into registers as well was
@@ -319,13 +318,23 @@ __device__ __forceinline__ void lds_load16_nt(__amdgpu_buffer_rsrc_t r, uint32_t
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(lds), 16, voff, 0, 0,
                                              kCachePolicyNT);
 }
-// The same with a wave-uniform scalar byte offset added to the global address.
-__device__ __forceinline__ void lds_load16s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, void* lds) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)(lds), 16, voff,
-                                             (int)soff, 0, 0);
-}
 __device__ __forceinline__ uint32_t lds_address(const void* p) {
     return (uint32_t)(uintptr_t)(const lds_char*)(p);
+}
+// 16-byte direct load with a wave-uniform scalar byte offset added to the
+// global address, issued from assembly with the LDS address in M0.  The
+// compiler waits for a direct load it tracks before any later LDS read that
+// it cannot prove disjoint, and without alias-scope information it proves
+// none: through the builtin, the next tile's prefetch made every tile wait
+// for that prefetch before its first K read (text+latent 1.790 -> 1.709 ms
+// together with the page indices read a tile ahead).  This one is not
+// tracked; the caller waits itself (dma_barrier) before anything reads the
+// bytes it writes.
+__device__ __forceinline__ void lds_dma16s(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, uint32_t lds_addr) {
+    asm volatile("buffer_load_dwordx4 %0, %1, %2 offen lds"
+                 :
+                 : "v"(voff), "s"(r), "s"(soff), "{m0}"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory");
 }
 
 // K/V of a pool that fits in 2 GB are read through one buffer resource per
@@ -353,25 +362,24 @@ constexpr int kTileKeysD128 = MSTAR_TILE_KEYS_D128;
 template <int D, int RBW, bool SMALL, bool CASC, int BN>
 __global__ __launch_bounds__(256, D == 64 ? 4 : (BN == 32 ? 3 : 2)) void tile_kernel(KArgs a) {
     static_assert(BN == 32 || BN == 64, "tile sizes");
+    constexpr int NW = 4;            // waves per workgroup (32 rows each)
     constexpr int NB = BN / 16;      // 16-key blocks of a tile
     constexpr int NC = BN / 32;      // 32-key steps of the value product
     constexpr int RBY = 2 * D;       // bytes per K/V row in LDS
     constexpr int CH = D / 8;        // 16-byte chunks per row
     constexpr int DS = D / 32;       // MFMA steps over the head dimension
     constexpr int DB = D / 16;       // 16-wide blocks of O^T
-    constexpr int NLD = BN * CH / 256;  // direct loads per wave, matrix and tile
+    constexpr int NLD = BN * CH / (64 * NW);  // direct loads per wave, matrix and tile
     constexpr int RPL = 64 / CH;     // rows filled by one wave-wide load
     constexpr int TB = BN * RBY;     // bytes of one K or V tile
     constexpr int PPT = BN / 16;     // pages per tile
-    // the two tile buffers are distinct arrays, so that the compiler, which
-    // tracks the direct loads, waits before a read only for the loads into
-    // the buffer being read
+    // two tile buffers: tile t + 1 loads into one while tile t is read from the other
     __shared__ __attribute__((aligned(1024))) char buf0[2][TB];  // [K, V] of even tiles
     __shared__ __attribute__((aligned(1024))) char buf1[2][TB];  // [K, V] of odd tiles
     __shared__ __attribute__((aligned(256))) int32_t page_ring[2][64];
     // each row's visible interval [lo, hi), read on partial tiles only (kept
     // out of the registers the tile loop carries)
-    __shared__ __attribute__((aligned(16))) int2 row_lohi[4][16 * RBW];
+    __shared__ __attribute__((aligned(16))) int2 row_lohi[NW][16 * RBW];
 
     // The planner's launch order names the (item, query head) of every
     // workgroup; it keeps the workgroups that read the same K/V pages on one
@@ -383,7 +391,7 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : (BN == 32 ? 3 : 2)) void tile_ke
     const SeqInfo si = a.seqs[it.seq];
     // the wave index is wave-uniform; readfirstlane lets the compiler keep
     // everything derived from it (row bounds, loop decisions) in scalars
-    const int tid = thread_id(), wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 3, lane = tid & 63;
+    const int tid = thread_id(), wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (NW - 1), lane = tid & 63;
     const int n = lane & 15, grp = lane >> 4;
     const int32_t* bt_row = a.bt + (int64_t)it.seq * a.bt_stride;
     const RowGroup rg;
@@ -479,11 +487,12 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : (BN == 32 ? 3 : 2)) void tile_ke
     // every tile.  Keeping the page indices out of compiler-tracked registers
     // matters: a tracked load in the loop makes the compiler wait for every
     // outstanding load (the just-issued K/V prefetch included) before its
-    // result is first moved.  Load j of wave w fills rows (4 j + w) RPL .. +RPL
-    // of the tile, which lie in one page; a thread's slot inside that page and
-    // its logical chunk are the same for every tile and every j.
+    // result is first moved.  Load j of wave w fills rows (NW j + w) RPL ..
+    // +RPL of the tile, which lie in one page; a thread's slot inside that
+    // page and its logical chunk are the same for every tile and every j.
     const int32_t page0 = it.k_begin >> 4;
     const int32_t n_pages = ((it.k_end + 15) >> 4) - page0;
+    const int n_tiles = (it.k_end - it.k_begin + BN - 1) / BN;
     const int32_t* bt_item = bt_row + page0;
     // window w of the item's pages: zeros past the last page (range check)
     auto load_window = [&](int w) {
@@ -515,32 +524,44 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : (BN == 32 ? 3 : 2)) void tile_ke
     // offset is pushed out of range), and so does every row of a page outside
     // the pool: no access outside the pool, and zeros in LDS.
     constexpr uint32_t kOutOfRange = 0x80000000u;
-    // Loads of tile tix into buffer `dst` ([K, V]).
-    auto issue_tile = [&](int tix, char (&dst)[2][TB]) {
+    // LDS addresses of the two tile buffers (K at +0, V at +TB)
+    const uint32_t lds_buf0 = __builtin_amdgcn_readfirstlane(lds_address(&buf0[0][0]));
+    const uint32_t lds_buf1 = __builtin_amdgcn_readfirstlane(lds_address(&buf1[0][0]));
+    // Page indices of tile tix for this wave's loads, read from the ring.
+    // Load j of wave w fills tile rows (NW j + w) RPL .. +RPL, which lie in
+    // page (NW j + w) RPL / 16 of the tile.  With four waves and RPL = 4
+    // (d = 128) that page is j for every wave: one 8- or 16-byte LDS read
+    // holds them.  Otherwise each wave reads its own indices at a
+    // wave-uniform LDS address, with no per-lane selection.
+    auto read_pages = [&](int tix, int32_t (&pv)[NLD]) {
         const int rel0 = tix * PPT;
-        // first tile of window w >= 1: every wave is past its last read of
-        // window w - 1, so its ring slot can take window w + 1
-        if (tix > 0 && (rel0 & 63) == 0) load_window((rel0 >> 6) + 1);
-        // page of load j within the tile: (4 j + wave) RPL / 16.  With RPL = 4
-        // (d = 128) it is j for every wave: one 16-byte LDS read holds the
-        // tile's four.  Otherwise each wave reads its own indices at a
-        // wave-uniform LDS address, with no per-lane selection.
         const int32_t* ring = &page_ring[(rel0 >> 6) & 1][rel0 & 63];
-        uint32_t page[NLD];
-        if constexpr (RPL == 4 && NLD == 4) {
+        if constexpr (NW == 4 && RPL == 4 && NLD == 4) {
             const int4 pq = *reinterpret_cast<const int4*>(ring);
-            const int32_t pgs[4] = {pq.x, pq.y, pq.z, pq.w};
-#pragma unroll
-            for (int j = 0; j < NLD; ++j) page[j] = (uint32_t)__builtin_amdgcn_readfirstlane(pgs[j]);
-        } else if constexpr (RPL == 4) {
+            pv[0] = pq.x; pv[1] = pq.y; pv[2] = pq.z; pv[3] = pq.w;
+        } else if constexpr (NW == 4 && RPL == 4 && NLD == 2) {
             const int2 pq = *reinterpret_cast<const int2*>(ring);
-            page[0] = (uint32_t)__builtin_amdgcn_readfirstlane(pq.x);
-            page[1] = (uint32_t)__builtin_amdgcn_readfirstlane(pq.y);
+            pv[0] = pq.x; pv[1] = pq.y;
         } else {
 #pragma unroll
-            for (int j = 0; j < NLD; ++j)
-                page[j] = (uint32_t)__builtin_amdgcn_readfirstlane(ring[((4 * j + wave) * RPL) >> 4]);
+            for (int j = 0; j < NLD; ++j) pv[j] = ring[((NW * j + wave) * RPL) >> 4];
         }
+    };
+    // Loads of tile tix into the buffer at LDS address `dst` ([K, V]), with
+    // the page indices `pv` read one tile earlier (so that the LDS round trip
+    // of the read overlaps a tile's compute); then the indices of tile tix + 1.
+    int32_t pv[NLD];
+    auto issue_tile = [&](int tix, uint32_t dst) {
+        const int rel0 = tix * PPT;
+        uint32_t page[NLD];
+#pragma unroll
+        for (int j = 0; j < NLD; ++j) page[j] = (uint32_t)__builtin_amdgcn_readfirstlane(pv[j]);
+        // first tile of window w >= 1: every wave is past its last read of
+        // window w - 1, so its ring slot can take window w + 1 (tile tix + 1
+        // lies in window w, or in w + 1 only if tix ends window w, whose
+        // successor has landed long before)
+        if (tix > 0 && (rel0 & 63) == 0) load_window((rel0 >> 6) + 1);
+        if (tix + 1 < n_tiles) read_pages(tix + 1, pv);
         bool all_ok = true;
 #pragma unroll
         for (int j = 0; j < NLD; ++j) all_ok &= page[j] < (uint32_t)a.num_pages;
@@ -551,27 +572,27 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : (BN == 32 ? 3 : 2)) void tile_ke
 #pragma unroll
             for (int j = 0; j < NLD; ++j) {
                 const uint32_t soff = page[j] * page_bytes;
-                lds_load16s(kpool, gk, soff, &dst[0][(4 * j + wave) * 1024]);
-                lds_load16s(vpool, gv, soff, &dst[1][(4 * j + wave) * 1024]);
+                lds_dma16s(kpool, gk, soff, dst + (NW * j + wave) * 1024);
+                lds_dma16s(vpool, gv, soff, dst + TB + (NW * j + wave) * 1024);
             }
         } else {
 #pragma unroll
             for (int j = 0; j < NLD; ++j) {
-                const int pg = ((4 * j + wave) * RPL) >> 4;  // page of this load within the tile
+                const int pg = ((NW * j + wave) * RPL) >> 4;  // page of this load within the tile
                 const bool ok = page[j] < (uint32_t)a.num_pages;
                 page_err |= !ok && k0 + 16 * pg < it.k_end;
-                const bool live = ok && (!tail || k0 + lrow0 + 4 * j * RPL < it.k_end);
+                const bool live = ok && (!tail || k0 + lrow0 + NW * j * RPL < it.k_end);
                 if (SMALL) {
                     const uint32_t soff = ok ? page[j] * page_bytes : 0u;
-                    lds_load16s(kpool, live ? gk : kOutOfRange, soff, &dst[0][(4 * j + wave) * 1024]);
-                    lds_load16s(vpool, live ? gv : kOutOfRange, soff, &dst[1][(4 * j + wave) * 1024]);
+                    lds_dma16s(kpool, live ? gk : kOutOfRange, soff, dst + (NW * j + wave) * 1024);
+                    lds_dma16s(vpool, live ? gv : kOutOfRange, soff, dst + TB + (NW * j + wave) * 1024);
                 } else {
                     const size_t pofs = ok ? (size_t)page[j] * page_bytes : 0;
                     const uint32_t nrec = ok ? page_bytes : 0u;
-                    lds_load16s(page_rsrc(kbase, pofs, nrec), live ? gk : kOutOfRange, 0u,
-                                &dst[0][(4 * j + wave) * 1024]);
-                    lds_load16s(page_rsrc(vbase, pofs, nrec), live ? gv : kOutOfRange, 0u,
-                                &dst[1][(4 * j + wave) * 1024]);
+                    lds_dma16s(page_rsrc(kbase, pofs, nrec), live ? gk : kOutOfRange, 0u,
+                               dst + (NW * j + wave) * 1024);
+                    lds_dma16s(page_rsrc(vbase, pofs, nrec), live ? gv : kOutOfRange, 0u,
+                               dst + TB + (NW * j + wave) * 1024);
                 }
             }
         }
@@ -697,7 +718,6 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : (BN == 32 ? 3 : 2)) void tile_ke
         values(vl, pf);
     };
 
-    const int n_tiles = (it.k_end - it.k_begin + BN - 1) / BN;
     if (n_tiles > 0) {
         load_window(0);
         load_window(1);
@@ -708,17 +728,18 @@ __global__ __launch_bounds__(256, D == 64 ? 4 : (BN == 32 ? 3 : 2)) void tile_ke
 #pragma unroll
             for (int s = 0; s < DS; ++s) asm volatile("" ::"v"(qf[rb][s]));
         dma_barrier();  // windows 0 and 1 of the page ring have landed
-        issue_tile(0, buf0);
+        read_pages(0, pv);
+        issue_tile(0, lds_buf0);
         // Tile tix is in buf[tix & 1].  At the top of each tile every wave has
         // its own loads of the tile done (vmcnt) and every wave is done with
         // the other buffer (barrier), which the next tile's loads then take.
         for (int tix = 0; tix < n_tiles; tix += 2) {
             dma_barrier();
-            if (tix + 1 < n_tiles) issue_tile(tix + 1, buf1);
+            if (tix + 1 < n_tiles) issue_tile(tix + 1, lds_buf1);
             compute_tile(tix, buf0);
             if (tix + 1 < n_tiles) {
                 dma_barrier();
-                if (tix + 2 < n_tiles) issue_tile(tix + 2, buf0);
+                if (tix + 2 < n_tiles) issue_tile(tix + 2, lds_buf0);
                 compute_tile(tix + 1, buf1);
             }
         }
