@@ -55,33 +55,14 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 struct RowIntervals {
     std::vector<int32_t> lo, hi;
-    std::vector<int64_t> lo_sum, hi_sum;  // prefix sums: lo_sum[i] = lo[0] + ... + lo[i-1]
 
-    void build_sums() {
-        lo_sum.assign(lo.size() + 1, 0);
-        hi_sum.assign(hi.size() + 1, 0);
-        for (size_t i = 0; i < lo.size(); ++i) {
-            lo_sum[i + 1] = lo_sum[i] + lo[i];
-            hi_sum[i + 1] = hi_sum[i] + hi[i];
-        }
-    }
-    // Visible (row, key) pairs of rows [r0, r1) inside keys [kb, ke), i.e. the
-    // sum over rows of max(0, min(hi, ke) - max(lo, kb)).  lo and hi never
-    // decrease from one row to the next and lo < hi, so the rows with a
-    // non-empty overlap are those from the first with hi > kb up to (not
-    // including) the first with lo >= ke, and on that range the min and the
-    // max each switch operand once: O(log rows) with the prefix sums.
+    // Visible (row, key) pairs of rows [r0, r1) inside keys [kb, ke): the sum
+    // over rows of max(0, min(hi, ke) - max(lo, kb)).  Items hold at most 128
+    // rows, so the direct sum is cheap.
     int64_t pairs(int32_t r0, int32_t r1, int32_t kb, int32_t ke) const {
-        if (r1 <= r0 || ke <= kb) return 0;
-        const auto H0 = hi.begin(), L0 = lo.begin();
-        const int32_t a = (int32_t)(std::upper_bound(H0 + r0, H0 + r1, kb) - H0);  // first hi > kb
-        const int32_t b = (int32_t)(std::lower_bound(L0 + r0, L0 + r1, ke) - L0);  // first lo >= ke
-        if (b <= a) return 0;
-        const int32_t c = (int32_t)(std::lower_bound(H0 + a, H0 + b, ke) - H0);    // first hi >= ke
-        const int32_t d = (int32_t)(std::lower_bound(L0 + a, L0 + b, kb) - L0);    // first lo >= kb
-        const int64_t sum_min_hi = (hi_sum[c] - hi_sum[a]) + (int64_t)ke * (b - c);
-        const int64_t sum_max_lo = (int64_t)kb * (d - a) + (lo_sum[b] - lo_sum[d]);
-        return sum_min_hi - sum_max_lo;
+        int64_t n = 0;
+        for (int32_t i = r0; i < r1; ++i) n += std::max(0, std::min(hi[i], ke) - std::max(lo[i], kb));
+        return n;
     }
 };
 
@@ -113,26 +94,27 @@ bool row_intervals(const mstar_seq_desc& s, const mstar_mask_spec& m, const msta
     }
     out.lo.resize(s.q_len);
     out.hi.resize(s.q_len);
-    int32_t k = 0;
+    int32_t k = -1;
+    int64_t seg_end = 0, blk_end = 0;  // end of the current segment and of the current block
     for (int32_t i = 0; i < s.q_len; ++i) {
         const int64_t p = (int64_t)s.kv_len - s.q_len + i;
-        while (k < m.seg_count) {
+        if (p >= seg_end) {  // the segment holding p (rows move forward one position at a time)
+            do {
+                ++k;
+                seg_end = (int64_t)segs[m.seg_begin + k].start + segs[m.seg_begin + k].len;
+            } while (p >= seg_end);
             const mstar_segment& g = segs[m.seg_begin + k];
-            if (p < (int64_t)g.start + g.len) break;
-            ++k;
+            blk_end = g.kind == MSTAR_SEG_BLOCKS ? g.start + ((p - g.start) / g.block + 1) * (int64_t)g.block : seg_end;
         }
-        const mstar_segment& g = segs[m.seg_begin + k];  // p lies inside g
-        const int64_t seg_end = (int64_t)g.start + g.len;
+        const mstar_segment& g = segs[m.seg_begin + k];
         int64_t hi;
         if (g.kind == MSTAR_SEG_CAUSAL) {
             hi = p + 1;
-        } else if (g.kind == MSTAR_SEG_FULL) {
-            hi = seg_end;
         } else {
-            hi = std::min<int64_t>(g.start + ((p - g.start) / g.block + 1) * (int64_t)g.block, seg_end);
+            if (p >= blk_end) blk_end += g.block;  // BLOCKS only: the next block (p advances by one)
+            hi = std::min<int64_t>(blk_end, seg_end);
         }
-        const int64_t lo = m.window > 0 ? std::max<int64_t>(0, p - m.window + 1) : 0;
-        out.lo[i] = (int32_t)lo;
+        out.lo[i] = m.window > 0 ? (int32_t)std::max<int64_t>(0, p - m.window + 1) : 0;
         out.hi[i] = (int32_t)hi;
     }
     return true;
@@ -286,6 +268,12 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     }
 
     plan.seqs.resize(num_seqs);
+    {
+        int64_t rows = 0;
+        for (int32_t r = 0; r < num_seqs; ++r) rows += seqs[r].q_len;
+        plan.row_hi.reserve((size_t)rows + 8);
+        plan.appends.reserve((size_t)(rows / kAppendRows + num_seqs));
+    }
     plan.key_lo.assign(num_seqs, 0);
     plan.key_hi.assign(num_seqs, 0);
     for (int32_t r = 0; r < num_seqs; ++r) {
@@ -556,7 +544,6 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     if (slot > INT32_MAX) { err = "too many partial rows"; return MSTAR_ERR_INVALID_ARG; }
 
     // ---- 5. longest first ------------------------------------------------------
-    for (RowIntervals& v : iv) v.build_sums();
     auto visible_in = [&](const WorkItem& w) -> int64_t {
         return iv[w.seq].pairs(w.row0, w.row0 + w.nrows, w.k_begin, w.k_end);
     };
@@ -585,73 +572,100 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     // the other XCDs idle).  Groups go to the least-loaded XCD, largest first;
     // inside a group the items keep their order.
     auto launch_order = [&](const std::vector<WorkItem>& items, bool per_head, std::vector<int32_t>& order) {
-        struct Group { int64_t cost = 0; int32_t kvh = 0; std::vector<int32_t> items; std::vector<int64_t> costs; };
-        std::vector<Group> whole, groups_;
-        std::vector<int64_t> index((size_t)num_seqs * P.num_kv_heads, -1);
+        // groups in order of first appearance; members flat, by group (a counting sort)
+        std::vector<int32_t> gid_of((size_t)num_seqs * P.num_kv_heads, -1);
+        std::vector<int32_t> g_kvh, g_count;
+        std::vector<int64_t> g_cost, item_cost(items.size());
         int64_t total = 0;
+        auto heads_of = [&](const WorkItem& w, int32_t& k0, int32_t& k1) {
+            k0 = per_head ? 0 : w.head;
+            k1 = per_head ? P.num_kv_heads : w.head + 1;
+        };
         for (size_t i = 0; i < items.size(); ++i) {
             const WorkItem& w = items[i];
             const int64_t pairs = per_head ? visible_in(w) * G : (int64_t)w.nrows * (w.k_end - w.k_begin);
-            for (int32_t kvh = 0; kvh < P.num_kv_heads; ++kvh) {
-                if (!per_head && kvh != w.head) continue;
-                int64_t& gi = index[(size_t)w.seq * P.num_kv_heads + kvh];
+            item_cost[i] = pairs + 1;  // +1: an empty item still costs a workgroup
+            int32_t k0, k1;
+            heads_of(w, k0, k1);
+            for (int32_t kvh = k0; kvh < k1; ++kvh) {
+                int32_t& gi = gid_of[(size_t)w.seq * P.num_kv_heads + kvh];
                 if (gi < 0) {
-                    gi = (int64_t)whole.size();
-                    whole.emplace_back();
-                    whole.back().kvh = kvh;
+                    gi = (int32_t)g_kvh.size();
+                    g_kvh.push_back(kvh);
+                    g_count.push_back(0);
+                    g_cost.push_back(0);
                 }
-                whole[gi].items.push_back((int32_t)i);
-                whole[gi].costs.push_back(pairs + 1);  // +1: an empty item still costs a workgroup
-                whole[gi].cost += pairs + 1;
+                ++g_count[gi];
+                g_cost[gi] += pairs + 1;
                 total += pairs + 1;
             }
         }
+        const size_t ng = g_kvh.size();
+        std::vector<int64_t> g_off(ng + 1, 0);
+        for (size_t g = 0; g < ng; ++g) g_off[g + 1] = g_off[g] + g_count[g];
+        std::vector<int32_t> members((size_t)g_off[ng]);
+        {
+            std::vector<int64_t> fill(g_off.begin(), g_off.end() - 1);
+            for (size_t i = 0; i < items.size(); ++i) {
+                int32_t k0, k1;
+                heads_of(items[i], k0, k1);
+                for (int32_t kvh = k0; kvh < k1; ++kvh)
+                    members[(size_t)fill[gid_of[(size_t)items[i].seq * P.num_kv_heads + kvh]]++] = (int32_t)i;
+            }
+        }
+        // pieces: whole groups, or consecutive runs of a group costlier than an
+        // even share of one XCD
         constexpr int kXcds = 8;
         const int64_t share = ceil_div(total, kXcds);
-        for (Group& g : whole) {
-            if (g.cost <= share) {
-                groups_.push_back(std::move(g));
+        struct Piece { int64_t cost, begin, end; int32_t kvh; };
+        std::vector<Piece> pieces;
+        pieces.reserve(ng);
+        for (size_t g = 0; g < ng; ++g) {
+            if (g_cost[g] <= share) {
+                pieces.push_back({g_cost[g], g_off[g], g_off[g + 1], g_kvh[g]});
                 continue;
             }
-            Group piece;
-            piece.kvh = g.kvh;
-            for (size_t k = 0; k < g.items.size(); ++k) {
-                if (!piece.items.empty() && piece.cost + g.costs[k] > share) {
-                    groups_.push_back(std::move(piece));
-                    piece = Group();
-                    piece.kvh = g.kvh;
+            Piece pc{0, g_off[g], g_off[g], g_kvh[g]};
+            for (int64_t k = g_off[g]; k < g_off[g + 1]; ++k) {
+                const int64_t c = item_cost[(size_t)members[(size_t)k]];
+                if (pc.end > pc.begin && pc.cost + c > share) {
+                    pieces.push_back(pc);
+                    pc = Piece{0, k, k, g_kvh[g]};
                 }
-                piece.items.push_back(g.items[k]);
-                piece.cost += g.costs[k];
+                pc.end = k + 1;
+                pc.cost += c;
             }
-            groups_.push_back(std::move(piece));
+            pieces.push_back(pc);
         }
-        std::stable_sort(groups_.begin(), groups_.end(), [](const Group& x, const Group& y) { return x.cost > y.cost; });
-        std::vector<int32_t> lists[kXcds];
+        std::stable_sort(pieces.begin(), pieces.end(), [](const Piece& x, const Piece& y) { return x.cost > y.cost; });
+        // each piece to the least-loaded XCD, then workgroup b of XCD x at launch slot 8 b + x
+        const int32_t hpi = per_head ? G : 1;  // workgroups per (item, KV head): its query heads, or the item
+        std::vector<int8_t> xcd_of(pieces.size());
         int64_t load[kXcds] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (const Group& g : groups_) {
+        size_t count[kXcds] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (size_t q = 0; q < pieces.size(); ++q) {
             int x = 0;
             for (int k = 1; k < kXcds; ++k)
                 if (load[k] < load[x]) x = k;
-            load[x] += g.cost;
-            for (int32_t item : g.items) {
-                const int32_t h0 = per_head ? g.kvh * G : g.kvh * G;
-                const int32_t h1 = per_head ? (g.kvh + 1) * G : g.kvh * G + 1;
-                for (int32_t h = h0; h < h1; ++h) {
-                    lists[x].push_back(item);
-                    lists[x].push_back(h);
-                }
-            }
+            load[x] += pieces[q].cost;
+            count[x] += (size_t)(pieces[q].end - pieces[q].begin) * hpi;
+            xcd_of[q] = (int8_t)x;
         }
         size_t slots = 0;
-        for (int x = 0; x < kXcds; ++x) slots = std::max(slots, lists[x].size() / 2);
+        for (int x = 0; x < kXcds; ++x) slots = std::max(slots, count[x]);
         if (slots * kXcds > (size_t)INT32_MAX / 2) return false;
         order.assign(2 * slots * kXcds, -1);  // padding workgroups exit at once
-        for (int x = 0; x < kXcds; ++x)
-            for (size_t k = 0; 2 * k < lists[x].size(); ++k) {
-                order[2 * (k * kXcds + x)] = lists[x][2 * k];
-                order[2 * (k * kXcds + x) + 1] = lists[x][2 * k + 1];
-            }
+        size_t pos[kXcds] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (size_t q = 0; q < pieces.size(); ++q) {
+            const int x = xcd_of[q];
+            const int32_t h0 = pieces[q].kvh * G;  // a cascade item's entry names the KV head's first query head
+            for (int64_t k = pieces[q].begin; k < pieces[q].end; ++k)
+                for (int32_t h = h0; h < h0 + hpi; ++h) {
+                    const size_t b = pos[x]++ * kXcds + x;
+                    order[2 * b] = members[(size_t)k];
+                    order[2 * b + 1] = h;
+                }
+        }
         return true;
     };
     if (!launch_order(plan.tiles, true, plan.tile_order) || !launch_order(plan.cascade, false, plan.casc_order)) {
