@@ -104,6 +104,37 @@ def test_determinism_and_page_permutation_bitwise():
     assert torch.equal(l1.view(torch.int32), l3.view(torch.int32))
 
 
+@pytest.mark.parametrize("flag", ["auto", "force_split"])
+@pytest.mark.parametrize("name", ["mixed", "serving_mix_bf16", "decode_bf16"])
+def test_repeated_launches_of_one_plan_write_every_output(name, flag):
+    """Launches of one plan back to back (the mixed batches run the few-row
+    kernel beside the tile kernel on the side stream), with the outputs
+    NaN-filled before each: every launch writes every output, and all agree
+    bitwise."""
+    import torch
+
+    b = W.reduced(name)
+    t = W.make_tensors_torch(b, DEV)
+    pl = plan_for(b, FLAGS[flag])
+    assert pl.stats()["decode_items"] > 0
+    q = t["q"]
+    bt = torch.from_numpy(np.ascontiguousarray(b.block_table)).to(DEV)
+    ws = attn.workspace(pl, DEV)
+    outs = []
+    for _ in range(6):
+        out = torch.full_like(q, float("nan"))
+        lse = torch.full((q.shape[0], b.num_qo_heads), float("nan"), dtype=torch.float32, device=DEV)
+        attn.fwd(pl, q, t["k_pages"], t["v_pages"], bt, out, lse, ws)
+        outs.append((out, lse))
+    torch.cuda.synchronize()
+    assert attn.check(pl) == 0
+    pl.destroy()
+    _compare(b, outs[0][0], outs[0][1], *_oracle(b, t), f"{name}/{flag} first launch")
+    for i, (o, l) in enumerate(outs[1:], 1):
+        assert torch.equal(o.view(torch.int16), outs[0][0].view(torch.int16)), f"launch {i}"
+        assert torch.equal(l.view(torch.int32), outs[0][1].view(torch.int32)), f"launch {i}"
+
+
 @pytest.mark.parametrize("name,cascade", [("mixed", False), ("serving_mix_bf16", False), ("mixed", True),
                                           ("decode_bf16", False)])
 def test_pool_beyond_2gb_takes_per_page_resources(name, cascade):
