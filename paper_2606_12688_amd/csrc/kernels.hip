@@ -799,8 +799,8 @@ __global__ __launch_bounds__(256, RB == 4 ? 1 : 2) void few_kernel(KArgs a) {
     constexpr int SB = SK * RBY;      // bytes of one wave's V slot
     static_assert(RB * 16 * D * 4 <= 4 * SB, "combine buffer must fit in one set of V slots");
     // V of the steps held in register buffers A and B goes straight from HBM
-    // into wave-private LDS slots (two arrays, so the compiler can tell which
-    // slot a read depends on and waits for exactly that slot's loads).
+    // into wave-private LDS slots, one array per buffer (the wave waits for
+    // all of its loads before each step; see compute_step).
     __shared__ __attribute__((aligned(1024))) char v_slot_a[4][SB];
     __shared__ __attribute__((aligned(1024))) char v_slot_b[4][SB];
     __shared__ float ml_lds[4][2][RB * 16];
