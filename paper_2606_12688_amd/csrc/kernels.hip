@@ -1126,9 +1126,14 @@ __global__ __launch_bounds__(256) void f32_kernel(KArgs a) {
     for (int32_t kb = lo; kb < hi; kb += 64) {
         const int32_t t = kb + lane;
         float s = kNegInf;
+        // this lane's key: its V row (page 0 for a bad page, whose key reads as zeros)
+        int32_t vrow = 0;
+        bool vok = false;
         if (t < hi) {
             const int32_t page = bt_row[t >> 4];
-            if ((uint32_t)page < (uint32_t)a.num_pages) {
+            vok = (uint32_t)page < (uint32_t)a.num_pages;
+            vrow = vok ? (page * 16 + (t & 15)) : 0;
+            if (vok) {
                 const float* kr = kg + (((int64_t)page * 16 + (t & 15)) * a.hkv + kvh) * D;
                 float dot = 0.0f;
                 for (int d = 0; d < D; d += 4) {
@@ -1154,15 +1159,26 @@ __global__ __launch_bounds__(256) void f32_kernel(KArgs a) {
         l = l * alpha + ps;
 #pragma unroll
         for (int e = 0; e < E; ++e) acc[e] *= alpha;
+        // weighted V rows: key j's probability and row come from lane j (a
+        // bad page's key contributes its probability to l and zeros to acc)
+        // (lanes past the last key hold probability 0 and row 0, so the keys
+        // go in groups of eight, whose loads are all in flight together)
+        const float pv = vok ? p : 0.0f;
         const int nk = min(64, hi - kb);
-        for (int j = 0; j < nk; ++j) {
-            const float pj = __shfl(p, j, 64);
-            const int32_t tj = kb + j;
-            const int32_t page = bt_row[tj >> 4];
-            if ((uint32_t)page >= (uint32_t)a.num_pages) continue;
-            const float* vr = vg + (((int64_t)page * 16 + (tj & 15)) * a.hkv + kvh) * D;
+        for (int j0 = 0; j0 < nk; j0 += 8) {
+            float vv[8][E], pj[8];
 #pragma unroll
-            for (int e = 0; e < E; ++e) acc[e] = fmaf(pj, vr[lane + 64 * e], acc[e]);
+            for (int u = 0; u < 8; ++u) {
+                pj[u] = __shfl(pv, j0 + u, 64);
+                const int32_t rj = __shfl(vrow, j0 + u, 64);
+                const float* vr = vg + ((int64_t)rj * a.hkv + kvh) * D;
+#pragma unroll
+                for (int e = 0; e < E; ++e) vv[u][e] = vr[lane + 64 * e];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+#pragma unroll
+                for (int e = 0; e < E; ++e) acc[e] = fmaf(pj[u], vv[u][e], acc[e]);
         }
         m = m_new;
     }
