@@ -53,23 +53,36 @@ namespace {
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// The visible interval [lo(i), hi(i)) of every query row of one request: hi
+// as stored in the plan's row_hi, lo from the window (a row at key position p
+// sees keys from p - window + 1 on; from 0 without a window).
 struct RowIntervals {
-    std::vector<int32_t> lo, hi;
+    const int32_t* hi_ = nullptr;
+    int64_t p0 = 0;  // key position of query row 0: kv_len - q_len
+    int32_t window = 0;
+
+    int32_t hi(int32_t i) const { return hi_[i]; }
+    int32_t lo(int32_t i) const { return window > 0 ? (int32_t)std::max<int64_t>(0, p0 + i - window + 1) : 0; }
 
     // Visible (row, key) pairs of rows [r0, r1) inside keys [kb, ke): the sum
     // over rows of max(0, min(hi, ke) - max(lo, kb)).  Items hold at most 128
     // rows, so the direct sum is cheap.
     int64_t pairs(int32_t r0, int32_t r1, int32_t kb, int32_t ke) const {
         int64_t n = 0;
-        for (int32_t i = r0; i < r1; ++i) n += std::max(0, std::min(hi[i], ke) - std::max(lo[i], kb));
+        if (window <= 0) {  // lo = 0 <= kb
+            for (int32_t i = r0; i < r1; ++i) n += std::max(0, std::min(hi_[i], ke) - kb);
+        } else {
+            for (int32_t i = r0; i < r1; ++i) n += std::max(0, std::min(hi_[i], ke) - std::max(lo(i), kb));
+        }
         return n;
     }
 };
 
-// Visible interval of every query row of one request.  Returns false (with a
+// Writes hi of every query row of one request to hi_out[0, q_len) and the
+// request's visible (row, key) pairs to pairs.  Returns false (with a
 // message) if the segments do not tile [0, kv_len) in order.
-bool row_intervals(const mstar_seq_desc& s, const mstar_mask_spec& m, const mstar_segment* segs,
-                   RowIntervals& out, std::string& err) {
+bool row_intervals(const mstar_seq_desc& s, const mstar_mask_spec& m, const mstar_segment* segs, int32_t* hi_out,
+                   int64_t& pairs, std::string& err) {
     // validate the tiling first
     int64_t pos = 0;
     for (int32_t k = 0; k < m.seg_count; ++k) {
@@ -92,8 +105,7 @@ bool row_intervals(const mstar_seq_desc& s, const mstar_mask_spec& m, const msta
         err = "segments must tile [0, kv_len) in order";
         return false;
     }
-    out.lo.resize(s.q_len);
-    out.hi.resize(s.q_len);
+    pairs = 0;
     int32_t k = -1;
     int64_t seg_end = 0, blk_end = 0;  // end of the current segment and of the current block
     for (int32_t i = 0; i < s.q_len; ++i) {
@@ -114,8 +126,9 @@ bool row_intervals(const mstar_seq_desc& s, const mstar_mask_spec& m, const msta
             if (p >= blk_end) blk_end += g.block;  // BLOCKS only: the next block (p advances by one)
             hi = std::min<int64_t>(blk_end, seg_end);
         }
-        out.lo[i] = m.window > 0 ? (int32_t)std::max<int64_t>(0, p - m.window + 1) : 0;
-        out.hi[i] = (int32_t)hi;
+        const int64_t lo = m.window > 0 ? std::max<int64_t>(0, p - m.window + 1) : 0;
+        hi_out[i] = (int32_t)hi;
+        pairs += hi - lo;
     }
     return true;
 }
@@ -172,7 +185,6 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
 
     // ---- 1. validate requests, 2. row intervals --------------------------
     std::vector<std::pair<int64_t, int64_t>> ranges;
-    std::vector<RowIntervals> iv(num_seqs);
     int64_t total_q = 0;
     for (int32_t r = 0; r < num_seqs; ++r) {
         const mstar_seq_desc& s = seqs[r];
@@ -198,12 +210,6 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             err = buf;
             return MSTAR_ERR_INVALID_ARG;
         }
-        std::string e2;
-        if (!row_intervals(s, m, segs, iv[r], e2)) {
-            snprintf(buf, sizeof buf, "request %d: ", r);
-            err = buf + e2;
-            return MSTAR_ERR_INVALID_ARG;
-        }
         if (s.q_len > 0) ranges.push_back({s.q_start, (int64_t)s.q_start + s.q_len});
         total_q = std::max<int64_t>(total_q, (int64_t)s.q_start + s.q_len);
     }
@@ -215,6 +221,48 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         }
     }
     plan.total_q = (int32_t)total_q;
+
+    // every request's rows (disjoint ranges below INT32_MAX / Hq): hi goes
+    // straight into row_hi, whose capacity is fixed here so the views stay valid
+    std::vector<RowIntervals> iv(num_seqs);
+    plan.seqs.resize(num_seqs);
+    {
+        int64_t rows = 0;
+        for (int32_t r = 0; r < num_seqs; ++r) rows += seqs[r].q_len;
+        plan.row_hi.reserve((size_t)rows + 8);
+        plan.appends.reserve((size_t)(rows / kAppendRows + num_seqs));
+    }
+    plan.key_lo.assign(num_seqs, 0);
+    plan.key_hi.assign(num_seqs, 0);
+    for (int32_t r = 0; r < num_seqs; ++r) {
+        const mstar_seq_desc& s = seqs[r];
+        SeqInfo& si = plan.seqs[r];
+        si.q_len = s.q_len;
+        si.kv_len = s.kv_len;
+        si.q_start = s.q_start;
+        si.window = masks[r].window;
+        si.hi_off = (int32_t)plan.row_hi.size();
+        si.seq_index = r;
+        si.pad0 = si.pad1 = 0;
+        plan.row_hi.resize(plan.row_hi.size() + s.q_len);
+        int32_t* hi = plan.row_hi.data() + si.hi_off;
+        int64_t pairs = 0;
+        std::string e2;
+        if (!row_intervals(s, masks[r], segs, hi, pairs, e2)) {
+            char buf[48];
+            snprintf(buf, sizeof buf, "request %d: ", r);
+            err = buf + e2;
+            return MSTAR_ERR_INVALID_ARG;
+        }
+        iv[r] = RowIntervals{hi, (int64_t)s.kv_len - s.q_len, masks[r].window};
+        plan.visible_pairs += pairs;
+        if (s.q_len > 0) {
+            plan.key_lo[r] = iv[r].lo(0);
+            plan.key_hi[r] = iv[r].hi(s.q_len - 1);
+        }
+    }
+    plan.visible_pairs *= P.num_qo_heads;
+    while (plan.row_hi.size() % 8) plan.row_hi.push_back(0);
 
     // ---- shared-prefix groups (cascade) ------------------------------------
     // group_of[r]: the group of request r or -1; member_rows[r]: query rows of
@@ -251,7 +299,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             // intervals never shrink from one row to the next: the first row
             // decides hi >= prefix_len, the last one lo == 0
             if (s.kv_len < gr.prefix_len ||
-                (s.q_len > 0 && (iv[r].hi[0] < gr.prefix_len || iv[r].lo[s.q_len - 1] != 0))) {
+                (s.q_len > 0 && (iv[r].hi(0) < gr.prefix_len || iv[r].lo(s.q_len - 1) != 0))) {
                 snprintf(buf, sizeof buf, "prefix group %d: a query row of request %d does not see the whole prefix",
                          g, r);
                 err = buf;
@@ -267,35 +315,6 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         }
     }
 
-    plan.seqs.resize(num_seqs);
-    {
-        int64_t rows = 0;
-        for (int32_t r = 0; r < num_seqs; ++r) rows += seqs[r].q_len;
-        plan.row_hi.reserve((size_t)rows + 8);
-        plan.appends.reserve((size_t)(rows / kAppendRows + num_seqs));
-    }
-    plan.key_lo.assign(num_seqs, 0);
-    plan.key_hi.assign(num_seqs, 0);
-    for (int32_t r = 0; r < num_seqs; ++r) {
-        const mstar_seq_desc& s = seqs[r];
-        SeqInfo& si = plan.seqs[r];
-        si.q_len = s.q_len;
-        si.kv_len = s.kv_len;
-        si.q_start = s.q_start;
-        si.window = masks[r].window;
-        si.hi_off = (int32_t)plan.row_hi.size();
-        si.seq_index = r;
-        si.pad0 = si.pad1 = 0;
-        plan.row_hi.insert(plan.row_hi.end(), iv[r].hi.begin(), iv[r].hi.end());
-        for (int32_t i = 0; i < s.q_len; ++i) plan.visible_pairs += (int64_t)(iv[r].hi[i] - iv[r].lo[i]);
-        if (s.q_len > 0) {
-            plan.key_lo[r] = iv[r].lo[0];
-            plan.key_hi[r] = iv[r].hi[s.q_len - 1];
-        }
-    }
-    plan.visible_pairs *= P.num_qo_heads;
-    while (plan.row_hi.size() % 8) plan.row_hi.push_back(0);
-
     // ---- 3. work units ----------------------------------------------------
     std::vector<Unit> few_units, tile_units;
     // (request, first row, rows) of member row tiles whose rows see no key past
@@ -310,7 +329,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             for (int32_t h = 0; h < P.num_qo_heads; ++h) {
                 for (int32_t row0 = 0; row0 < s.q_len; row0 += kF32Rows) {
                     const int32_t nr = std::min(kF32Rows, s.q_len - row0);
-                    WorkItem w{r, h, row0, nr, align_down16(v.lo[row0]), v.hi[row0 + nr - 1], -1, -1};
+                    WorkItem w{r, h, row0, nr, align_down16(v.lo(row0)), v.hi(row0 + nr - 1), -1, -1};
                     plan.f32.push_back(w);
                 }
             }
@@ -320,7 +339,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         // a cascade member's own work covers the keys after the shared prefix
         const bool member = group_of[r] >= 0;
         const int32_t own0 = member ? groups[group_of[r]].prefix_len : 0;
-        if (member && v.hi[s.q_len - 1] <= own0) continue;  // the prefix is all it sees
+        if (member && v.hi(s.q_len - 1) <= own0) continue;  // the prefix is all it sees
         if (R <= kDecodeMaxRows) {
             // at d = 128 a unit holds at most 32 rows: the 64-row instance of
             // the few-row kernel does not fit its registers
@@ -329,7 +348,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
                 for (int32_t rr0 = 0; rr0 < R; rr0 += span) {
                     const int32_t nr = std::min<int32_t>(span, (int32_t)R - rr0);
                     const int32_t q0 = rr0 / G, q1 = (rr0 + nr - 1) / G;
-                    Unit u{r, kvh, rr0, nr, member ? own0 : align_down16(v.lo[q0]), v.hi[q1], 0};
+                    Unit u{r, kvh, rr0, nr, member ? own0 : align_down16(v.lo(q0)), v.hi(q1), 0};
                     // a member unit whose rows see only the prefix keeps an
                     // empty own range (it writes empty partials for the merge)
                     u.k_end = std::max(u.k_end, u.k_begin);
@@ -343,8 +362,8 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             // one unit per row tile, shared by every query head
             for (int32_t row0 = 0; row0 < s.q_len; row0 += kTileRows) {
                 const int32_t nr = std::min(kTileRows, s.q_len - row0);
-                const int32_t kb = member ? own0 : align_down16(v.lo[row0]);
-                const int32_t ke = v.hi[row0 + nr - 1];
+                const int32_t kb = member ? own0 : align_down16(v.lo(row0));
+                const int32_t ke = v.hi(row0 + nr - 1);
                 if (ke <= kb) {  // rows that see only the prefix (members only: kb = 0 otherwise)
                     if (member) prefix_only.push_back({r, row0, nr});
                     continue;
@@ -449,7 +468,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     };
     for (int32_t r = 0; r < num_seqs; ++r) {
         if (group_of[r] < 0 || seqs[r].q_len == 0) continue;
-        if (iv[r].hi[seqs[r].q_len - 1] > groups[group_of[r]].prefix_len) continue;
+        if (iv[r].hi(seqs[r].q_len - 1) > groups[group_of[r]].prefix_len) continue;
         prefix_only_rows(r, 0, seqs[r].q_len);
     }
     for (const RowRun& run : prefix_only) prefix_only_rows(run.seq, run.row0, run.row0 + run.nrows);
@@ -547,7 +566,8 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     auto visible_in = [&](const WorkItem& w) -> int64_t {
         return iv[w.seq].pairs(w.row0, w.row0 + w.nrows, w.k_begin, w.k_end);
     };
-    auto lpt = [&](std::vector<WorkItem>& items, bool by_pairs) {
+    // sorts items by decreasing key; `keys` (if given) receives the keys in the new order
+    auto lpt = [&](std::vector<WorkItem>& items, bool by_pairs, std::vector<int64_t>* keys) {
         std::vector<std::pair<int64_t, int32_t>> key(items.size());
         for (size_t i = 0; i < items.size(); ++i)
             key[i] = {by_pairs ? visible_in(items[i]) : (int64_t)(items[i].k_end - items[i].k_begin), (int32_t)i};
@@ -555,10 +575,15 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         std::vector<WorkItem> sorted(items.size());
         for (size_t i = 0; i < items.size(); ++i) sorted[i] = items[key[i].second];
         items.swap(sorted);
+        if (keys) {
+            keys->resize(key.size());
+            for (size_t i = 0; i < key.size(); ++i) (*keys)[i] = key[i].first;
+        }
     };
-    lpt(plan.tiles, true);
-    lpt(plan.few, false);
-    lpt(plan.f32, true);
+    std::vector<int64_t> tile_pairs;  // visible pairs of each tile item, for the launch order
+    lpt(plan.tiles, true, &tile_pairs);
+    lpt(plan.few, false, nullptr);
+    lpt(plan.f32, true, nullptr);
 
     // ---- 6. launch order of the multi-row workgroups ----------------------------
     // One workgroup per (tile item, query head); one per cascade item (its rows
@@ -571,7 +596,8 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     // consecutive runs of items (one such group alone would otherwise leave
     // the other XCDs idle).  Groups go to the least-loaded XCD, largest first;
     // inside a group the items keep their order.
-    auto launch_order = [&](const std::vector<WorkItem>& items, bool per_head, std::vector<int32_t>& order) {
+    auto launch_order = [&](const std::vector<WorkItem>& items, bool per_head, const std::vector<int64_t>* pairs_of,
+                            std::vector<int32_t>& order) {
         // groups in order of first appearance; members flat, by group (a counting sort)
         std::vector<int32_t> gid_of((size_t)num_seqs * P.num_kv_heads, -1);
         std::vector<int32_t> g_kvh, g_count;
@@ -583,7 +609,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         };
         for (size_t i = 0; i < items.size(); ++i) {
             const WorkItem& w = items[i];
-            const int64_t pairs = per_head ? visible_in(w) * G : (int64_t)w.nrows * (w.k_end - w.k_begin);
+            const int64_t pairs = per_head ? (*pairs_of)[i] * G : (int64_t)w.nrows * (w.k_end - w.k_begin);
             item_cost[i] = pairs + 1;  // +1: an empty item still costs a workgroup
             int32_t k0, k1;
             heads_of(w, k0, k1);
@@ -668,7 +694,8 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         }
         return true;
     };
-    if (!launch_order(plan.tiles, true, plan.tile_order) || !launch_order(plan.cascade, false, plan.casc_order)) {
+    if (!launch_order(plan.tiles, true, &tile_pairs, plan.tile_order) ||
+        !launch_order(plan.cascade, false, nullptr, plan.casc_order)) {
         err = "too many tile workgroups";
         return MSTAR_ERR_INVALID_ARG;
     }
