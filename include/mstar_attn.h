@@ -164,7 +164,9 @@ typedef struct {
  * plan larger than every pooled buffer, allocate (hipMalloc, hipHostMalloc,
  * hipStreamCreate); steady-state planning allocates no device memory and
  * makes no device-synchronizing call.  A pooled buffer's upload first waits,
- * on `upload_stream`, for the work its previous plan enqueued.  On success
+ * on `upload_stream`, for the work its previous plan enqueued.  The host-side
+ * item lists are pooled too (up to 8 sets, none over 64 MB), so that a plan
+ * writes into memory an earlier plan has already touched.  On success
  * *out is a new plan; on failure *out is NULL.
  * Errors: INVALID_ARG (null pointer, Hq % Hkv != 0, q_len > kv_len, segments
  * not tiling [0, kv_len), negative window, kv_len > 16 * max_blocks_per_seq,
@@ -374,7 +376,8 @@ void mstar_planner_destroy(mstar_planner_t* planner);
 int mstar_kv_append(const mstar_plan_t* plan, const void* k_new, const void* v_new, const int32_t* block_table,
                     void* k_pages, void* v_pages, hipStream_t stream);
 
-/* Release the plan: its host memory is freed and its device buffers, staging
+/* Release the plan: its host item lists go back to the host pool (or are
+ * freed) and its device buffers, staging
  * copy, events and side stream go back to the per-device pool (no HIP call,
  * no device synchronization).  The work of the plan's last fwd or kv_append
  * call enqueued outside graph capture may still be running: a later plan that

@@ -113,6 +113,29 @@ void release_block(PlanBlock* b) {
     free_block(b);
 }
 
+// Host halves of plans are pooled the same way: a destroyed plan's item
+// lists keep their capacity for a later plan, which then writes into memory
+// it has already touched (on large batches the first-touch page faults of
+// fresh multi-megabyte lists cost more than the planning).  At most
+// kHostPoolMax are kept, and none holding more than kHostPoolMaxBytes.
+constexpr size_t kHostPoolMax = 8;
+constexpr size_t kHostPoolMaxBytes = 64 << 20;
+std::mutex g_host_mu;
+std::vector<mstar::HostPlan> g_host_pool;
+
+void take_host(mstar::HostPlan& h) {
+    std::lock_guard<std::mutex> lk(g_host_mu);
+    if (g_host_pool.empty()) return;
+    h = std::move(g_host_pool.back());
+    g_host_pool.pop_back();
+}
+
+void give_host(mstar::HostPlan& h) {
+    if (h.capacity_bytes() > kHostPoolMaxBytes) return;
+    std::lock_guard<std::mutex> lk(g_host_mu);
+    if (g_host_pool.size() < kHostPoolMax) g_host_pool.push_back(std::move(h));
+}
+
 }  // namespace
 
 struct mstar_plan {
@@ -181,6 +204,7 @@ static int plan_impl(const mstar_attn_params* params, const mstar_seq_desc* seqs
 
     mstar_plan* plan = new (std::nothrow) mstar_plan();
     if (!plan) return fail(MSTAR_ERR_NOMEM, "host allocation failed");
+    take_host(plan->host);
     std::string err;
     int rc;
     try {
@@ -593,6 +617,7 @@ MSTAR_EXPORT int mstar_attn_plan_cascade_order(const mstar_plan_t* plan, int32_t
 MSTAR_EXPORT void mstar_attn_plan_destroy(mstar_plan_t* plan) {
     if (!plan) return;
     release_block(plan->blk);  // back to the pool: no HIP call, no device synchronization
+    give_host(plan->host);
     delete plan;
 }
 

@@ -176,7 +176,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         return MSTAR_ERR_INVALID_ARG;
     }
 
-    plan = HostPlan();
+    plan.reset();
     plan.params = P;
     plan.num_seqs = num_seqs;
     const int32_t G = P.num_qo_heads / P.num_kv_heads;
@@ -574,7 +574,7 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         std::stable_sort(key.begin(), key.end(), [](const auto& a, const auto& b) { return a.first > b.first; });
         std::vector<WorkItem> sorted(items.size());
         for (size_t i = 0; i < items.size(); ++i) sorted[i] = items[key[i].second];
-        items.swap(sorted);
+        std::copy(sorted.begin(), sorted.end(), items.begin());  // items keeps its buffer
         if (keys) {
             keys->resize(key.size());
             for (size_t i = 0; i < key.size(); ++i) (*keys)[i] = key[i].first;

@@ -34,6 +34,27 @@ struct HostPlan {
     std::vector<int32_t> casc_order;
     int64_t visible_pairs = 0;
     int64_t partial_slots = 0;
+
+    // Back to the state of a new HostPlan, keeping the vectors' capacity (a
+    // pooled plan then writes into memory it has already touched).  Every
+    // member above is reset here.
+    void reset() {
+        params = mstar_attn_params{};
+        num_seqs = total_q = 0;
+        group = decode_rb = 1;
+        for (auto* v : {&row_hi, &key_lo, &key_hi, &tile_order, &casc_rows, &casc_order}) v->clear();
+        for (auto* v : {&tiles, &few, &f32, &appends, &cascade}) v->clear();
+        seqs.clear();
+        merges.clear();
+        visible_pairs = partial_slots = 0;
+    }
+    // Bytes the vectors hold (their capacity).
+    size_t capacity_bytes() const {
+        size_t n = seqs.capacity() * sizeof(SeqInfo) + merges.capacity() * sizeof(MergeItem);
+        for (auto* v : {&row_hi, &key_lo, &key_hi, &tile_order, &casc_rows, &casc_order}) n += v->capacity() * 4;
+        for (auto* v : {&tiles, &few, &f32, &appends, &cascade}) n += v->capacity() * sizeof(WorkItem);
+        return n;
+    }
 };
 
 // Fills `plan` from the descriptors.  Returns MSTAR_OK or an MSTAR_ERR_* code

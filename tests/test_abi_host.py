@@ -447,3 +447,31 @@ def test_noalloc_entry_point_refuses_plans_beyond_its_scratch_on_the_host():
     assert L.mstar_attn_fwd_noalloc(pl.handle, 16, 16, 16, 16, 16, 16, None) == attn.ERR_INVALID_ARG
     assert "host-only" in attn.last_error()
     pl.destroy()
+
+
+def _plan_record(pl):
+    st = pl.stats()
+    st.pop("plan_host_us")
+    return (sorted(st.items()), [pl.items(k).tolist() for k in range(6)], pl.tile_order().tolist(),
+            pl.tile_order(True).tolist(), pl.key_ranges().tolist())
+
+
+def test_plans_built_on_recycled_host_lists_equal_fresh_ones():
+    """Destroyed plans hand their host lists (capacity kept) to later plans:
+    a plan built on the lists of a larger or different plan (tiles, few-row
+    items, fp32 items, merges, a cascade) equals the same plan built while
+    those lists were held by live plans."""
+    batches = [(W.reduced("rollout_bf16"), 0, False), (W.reduced("mixed"), attn.FLAG_FORCE_SPLIT, False),
+               (W.reduced("decode_bf16"), 0, False), (W.reduced("tiny_causal_f32"), 0, False),
+               (W.reduced("shared_prefix_decode_bf16"), 0, True)]
+    # reference records while every plan stays alive (no list is recycled between them)
+    live = [plan_for(b, f | attn.FLAG_HOST_ONLY, cascade=c) for b, f, c in batches]
+    ref = [_plan_record(p) for p in live]
+    for p in live:
+        p.destroy()
+    for order in (range(len(batches)), reversed(range(len(batches)))):
+        for i in order:
+            b, f, c = batches[i]
+            pl = plan_for(b, f | attn.FLAG_HOST_ONLY, cascade=c)
+            assert _plan_record(pl) == ref[i], b.name
+            pl.destroy()  # its lists go to the next plan
