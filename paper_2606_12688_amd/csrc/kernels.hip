@@ -131,18 +131,9 @@ __device__ __forceinline__ void row_interval(const KArgs& a, const SeqInfo& si, 
     hi = min(h0, it.k_end);
 }
 
-// Online-softmax update of one 16-row block with NB 16-key blocks of raw
-// scores (hidden keys already -inf).  m and l are kept in base-2 units of the
-// scaled scores: c = sm_scale * log2(e) > 0, so max(c s) = c max(s) and every
-// probability is one FMA and one exp2.
-//
-// The reference max m is refreshed lazily: only when some row of the wave
-// sees its max grow by more than kLazy (or has no reference yet).  Otherwise
-// probabilities are taken against the stale m, so they stay below 2^kLazy, and
-// the rescale of the O accumulators (the most expensive VALU work per tile)
-// is skipped.  The result is exact either way: out = O / l and
-// lse = m + log2(l) use the same reference.  Returns true (wave-uniform) when
-// O must be multiplied by `alpha`.  Leaves the probabilities in s.
+// Lazy reference threshold (base-2 units): the online softmax moves its
+// reference max only when a row's max exceeds it by more than this, so
+// probabilities taken against a stale reference stay below 2^kLazy.
 constexpr float kLazy = 8.0f;
 
 // Balanced reductions over the 4*NB score values a lane holds for one row.
