@@ -77,12 +77,15 @@ def _compare_requests(b, t, out, lse, reqs, key_ranges, label):
     return compare(b, out.index_select(0, idx), lse.index_select(0, idx), ro, rl, label)
 
 
-@pytest.mark.parametrize("name", ["tiny_causal_f32", "decode_bf16", "stream_window_bf16"])
-def test_full_size_launch_every_output(name):
+# configurations 1 and 2 also at seeds 1 and 2 (new values and page permutation; new lengths for decode)
+@pytest.mark.parametrize("name,seed", [("tiny_causal_f32", 0), ("tiny_causal_f32", 1), ("tiny_causal_f32", 2),
+                                       ("decode_bf16", 0), ("decode_bf16", 1), ("decode_bf16", 2),
+                                       ("stream_window_bf16", 0)])
+def test_full_size_launch_every_output(name, seed):
     import torch
 
-    b = W.FULL_SIZE[name]()
-    print(f"{name}: generating", flush=True)
+    b = W.FULL_SIZE[name](seed)
+    print(f"{name} seed {seed}: generating", flush=True)
     t = W.make_tensors_torch(b, DEV)
     out, lse = run_gpu(b, t)
     torch.cuda.synchronize()
@@ -93,7 +96,8 @@ def test_full_size_launch_every_output(name):
     for chunk in np.array_split(np.arange(b.num_seqs), max(1, b.num_seqs // 32)):
         eo, el = _compare_requests(b, t, out, lse, chunk, kr[chunk], f"{name} requests {chunk[0]}..{chunk[-1]}")
         worst = [max(worst[0], eo), max(worst[1], el)]
-    print(f"{name} full launch, every output: max|dout|={worst[0]:.3e} max|dlse|={worst[1]:.3e}", flush=True)
+    print(f"{name} seed {seed} full launch, every output: max|dout|={worst[0]:.3e} max|dlse|={worst[1]:.3e}",
+          flush=True)
 
 
 @pytest.mark.parametrize("name,which", [("text_latent_bf16", "first"), ("text_latent_bf16", "last"),
