@@ -105,30 +105,40 @@ bool row_intervals(const mstar_seq_desc& s, const mstar_mask_spec& m, const msta
         err = "segments must tile [0, kv_len) in order";
         return false;
     }
+    // Rows come in runs over which hi is constant (a FULL segment, one block
+    // of a BLOCKS segment) or grows by one per row (CAUSAL): each run is
+    // filled in one pass and its pair count summed in closed form.
     pairs = 0;
-    int32_t k = -1;
-    int64_t seg_end = 0, blk_end = 0;  // end of the current segment and of the current block
-    for (int32_t i = 0; i < s.q_len; ++i) {
-        const int64_t p = (int64_t)s.kv_len - s.q_len + i;
-        if (p >= seg_end) {  // the segment holding p (rows move forward one position at a time)
-            do {
-                ++k;
-                seg_end = (int64_t)segs[m.seg_begin + k].start + segs[m.seg_begin + k].len;
-            } while (p >= seg_end);
-            const mstar_segment& g = segs[m.seg_begin + k];
-            blk_end = g.kind == MSTAR_SEG_BLOCKS ? g.start + ((p - g.start) / g.block + 1) * (int64_t)g.block : seg_end;
-        }
+    const int64_t p0 = (int64_t)s.kv_len - s.q_len;  // key position of query row 0
+    const int64_t W = m.window;
+    // sum over positions p in [pa, pb) of lo(p) = max(0, p - W + 1) (0 without a window)
+    auto lo_sum = [&](int64_t pa, int64_t pb) -> int64_t {
+        if (W <= 0) return 0;
+        const int64_t a = std::max(pa, W - 1);
+        if (a >= pb) return 0;
+        const int64_t first = a - W + 1, last = pb - W;  // lo of positions a and pb - 1
+        return (first + last) * (pb - a) / 2;
+    };
+    int32_t k = 0;
+    int32_t i = 0;
+    while (i < s.q_len) {
+        const int64_t p = p0 + i;
+        while ((int64_t)segs[m.seg_begin + k].start + segs[m.seg_begin + k].len <= p) ++k;  // segment holding p
         const mstar_segment& g = segs[m.seg_begin + k];
-        int64_t hi;
+        const int64_t seg_end = (int64_t)g.start + g.len;
+        int64_t run_end = seg_end;  // position after the run
+        if (g.kind == MSTAR_SEG_BLOCKS)
+            run_end = std::min<int64_t>(g.start + ((p - g.start) / g.block + 1) * (int64_t)g.block, seg_end);
+        const int32_t n = (int32_t)std::min<int64_t>(run_end - p, (int64_t)s.q_len - i);
         if (g.kind == MSTAR_SEG_CAUSAL) {
-            hi = p + 1;
+            for (int32_t r = 0; r < n; ++r) hi_out[i + r] = (int32_t)(p + 1 + r);  // hi = p + 1
+            pairs += (2 * (p + 1) + n - 1) * n / 2;
         } else {
-            if (p >= blk_end) blk_end += g.block;  // BLOCKS only: the next block (p advances by one)
-            hi = std::min<int64_t>(blk_end, seg_end);
+            std::fill(hi_out + i, hi_out + i + n, (int32_t)run_end);  // the end of the block or segment
+            pairs += run_end * n;
         }
-        const int64_t lo = m.window > 0 ? std::max<int64_t>(0, p - m.window + 1) : 0;
-        hi_out[i] = (int32_t)hi;
-        pairs += hi - lo;
+        pairs -= lo_sum(p, p + n);
+        i += n;
     }
     return true;
 }
