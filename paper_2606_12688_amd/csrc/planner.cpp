@@ -68,6 +68,10 @@ struct RowIntervals {
     // over rows of max(0, min(hi, ke) - max(lo, kb)).  Items hold at most 128
     // rows, so the direct sum is cheap.
     int64_t pairs(int32_t r0, int32_t r1, int32_t kb, int32_t ke) const {
+        if (r1 <= r0 || ke <= kb) return 0;
+        // hi and lo never decrease from one row to the next: when the first row
+        // reaches ke and the last starts at or below kb, every row sees [kb, ke)
+        if (hi_[r0] >= ke && lo(r1 - 1) <= kb) return (int64_t)(r1 - r0) * (ke - kb);
         int64_t n = 0;
         if (window <= 0) {  // lo = 0 <= kb
             for (int32_t i = r0; i < r1; ++i) n += std::max(0, std::min(hi_[i], ke) - kb);
@@ -581,7 +585,9 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
         std::vector<std::pair<int64_t, int32_t>> key(items.size());
         for (size_t i = 0; i < items.size(); ++i)
             key[i] = {by_pairs ? visible_in(items[i]) : (int64_t)(items[i].k_end - items[i].k_begin), (int32_t)i};
-        std::stable_sort(key.begin(), key.end(), [](const auto& a, const auto& b) { return a.first > b.first; });
+        // decreasing key, equal keys in their original order (no merge buffer, unlike a stable sort)
+        std::sort(key.begin(), key.end(),
+                  [](const auto& a, const auto& b) { return a.first != b.first ? a.first > b.first : a.second < b.second; });
         std::vector<WorkItem> sorted(items.size());
         for (size_t i = 0; i < items.size(); ++i) sorted[i] = items[key[i].second];
         std::copy(sorted.begin(), sorted.end(), items.begin());  // items keeps its buffer
@@ -673,7 +679,10 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
             }
             pieces.push_back(pc);
         }
-        std::stable_sort(pieces.begin(), pieces.end(), [](const Piece& x, const Piece& y) { return x.cost > y.cost; });
+        // costliest first, equal costs in creation order (begin grows with it)
+        std::sort(pieces.begin(), pieces.end(), [](const Piece& x, const Piece& y) {
+            return x.cost != y.cost ? x.cost > y.cost : x.begin < y.begin;
+        });
         // each piece to the least-loaded XCD, then workgroup b of XCD x at launch slot 8 b + x
         const int32_t hpi = per_head ? G : 1;  // workgroups per (item, KV head): its query heads, or the item
         std::vector<int8_t> xcd_of(pieces.size());
