@@ -390,12 +390,18 @@ int build_host_plan(const mstar_attn_params* params, const mstar_seq_desc* seqs,
     }
 
     // KV append items: the new rows of each request in chunks of kAppendRows
-    for (int32_t r = 0; r < num_seqs; ++r) {
-        const mstar_seq_desc& s = seqs[r];
-        for (int32_t row0 = 0; row0 < s.q_len; row0 += kAppendRows) {
-            const int32_t nr = std::min(kAppendRows, s.q_len - row0);
-            plan.appends.push_back(WorkItem{r, -1, row0, nr, s.kv_len - s.q_len + row0, s.kv_len - s.q_len + row0 + nr,
-                                            -1, -1});
+    {
+        size_t n_app = 0;
+        for (int32_t r = 0; r < num_seqs; ++r) n_app += (size_t)ceil_div(seqs[r].q_len, kAppendRows);
+        plan.appends.resize(n_app);
+        WorkItem* w = plan.appends.data();
+        for (int32_t r = 0; r < num_seqs; ++r) {
+            const mstar_seq_desc& s = seqs[r];
+            const int32_t p0 = s.kv_len - s.q_len;
+            for (int32_t row0 = 0; row0 < s.q_len; row0 += kAppendRows) {
+                const int32_t nr = std::min(kAppendRows, s.q_len - row0);
+                *w++ = WorkItem{r, -1, row0, nr, p0 + row0, p0 + row0 + nr, -1, -1};
+            }
         }
     }
 
