@@ -441,8 +441,8 @@ def main():
                     help="run only a plain 1 GiB device copy (for HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the attention shards by request or KV head with no exchange; see DESIGN.md).", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path (the attention would "
+              "shard by request or by KV head, each GPU running its share with no exchange).", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -1,7 +1,7 @@
 // Host-only stand-ins for the kernel launchers, for the sanitizer build of the
 // library's host code (planner and C-ABI), which the CPU tests load instead of
 // the HIP build: every launch reports hipErrorNotSupported, so a device call
-// through this build fails loudly instead of computing anything.
+// through the sanitizer build fails loudly instead of computing anything.
 #include "kernels.h"
 
 namespace mstar {
