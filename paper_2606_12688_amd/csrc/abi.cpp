@@ -180,12 +180,6 @@ hipError_t mark_use(const mstar_plan* plan, hipStream_t s) {
     return e;
 }
 
-template <typename T>
-size_t put(unsigned char* blob, size_t off, const std::vector<T>& v) {
-    if (!v.empty()) std::memcpy(blob + off, v.data(), v.size() * sizeof(T));
-    return off;
-}
-
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 }  // namespace
@@ -264,18 +258,27 @@ static int plan_impl(const mstar_attn_params* params, const mstar_seq_desc* seqs
         if (b->uploaded_set && (e = hipEventSynchronize(b->uploaded)) != hipSuccess)
             return give_up(e, "hipEventSynchronize(plan staging)");
         unsigned char* blob = static_cast<unsigned char*>(b->pinned);
-        std::memset(blob, 0, plan->bytes);
-        put(blob, plan->off_seqs, h.seqs);
-        put(blob, plan->off_row_hi, h.row_hi);
-        put(blob, plan->off_tiles, h.tiles);
-        put(blob, plan->off_order, h.tile_order);
-        put(blob, plan->off_few, h.few);
-        put(blob, plan->off_f32, h.f32);
-        put(blob, plan->off_merge, h.merges);
-        put(blob, plan->off_append, h.appends);
-        put(blob, plan->off_casc, h.cascade);
-        put(blob, plan->off_casc_rows, h.casc_rows);
-        put(blob, plan->off_casc_order, h.casc_order);
+        // the sections in layout order; only the alignment gaps between them
+        // and the tail (the error word) are zeroed
+        size_t pos = 0;
+        auto put = [&](size_t off, const auto& v) {
+            if (off > pos) std::memset(blob + pos, 0, off - pos);
+            const size_t n = v.size() * sizeof(v[0]);
+            if (n) std::memcpy(blob + off, v.data(), n);
+            pos = off + n;
+        };
+        put(plan->off_seqs, h.seqs);
+        put(plan->off_row_hi, h.row_hi);
+        put(plan->off_tiles, h.tiles);
+        put(plan->off_order, h.tile_order);
+        put(plan->off_few, h.few);
+        put(plan->off_f32, h.f32);
+        put(plan->off_merge, h.merges);
+        put(plan->off_append, h.appends);
+        put(plan->off_casc, h.cascade);
+        put(plan->off_casc_rows, h.casc_rows);
+        put(plan->off_casc_order, h.casc_order);
+        std::memset(blob + pos, 0, plan->bytes - pos);
         // ... and work of the block's previous plan that reads the device copy
         // must be done before the upload overwrites it (a device-side wait)
         if (b->last_use_set && (e = hipStreamWaitEvent(up, b->last_use, 0)) != hipSuccess)
