@@ -1,0 +1,62 @@
+"""GPU parity at the extremes of the batch descriptors, every output against
+the oracle:
+
+- query-head groups much larger than a 16-row MFMA block (28, 32 and 64
+  query heads per KV head): one decode token is then 28-64 rows of few-row
+  units, a 16-token chunk is 448-1024 rows and goes to the tile path, and
+  the row -> (query row, head) mapping wraps inside every 16-row block;
+- items far longer than the long-item tests: a 130-row prefill over 40000
+  keys (the tile kernel's page-index ring refills about twenty times), a
+  decode token over 60000 keys (the few-row kernel's page-index register
+  window moves a dozen times) and a 64-row chunk under a 20000-key window
+  over 50000 keys, planned without key splitting so that each stays one
+  item, and with the default policy."""
+import pytest
+
+import workloads as W
+from paper_2606_12688_amd import attn
+from tests.helpers import compare, oracle_of, run_gpu
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+FLAGS = {"auto": 0, "force_split": attn.FLAG_FORCE_SPLIT, "no_split": attn.FLAG_NO_SPLIT}
+C, FULL = W.SEG_CAUSAL, W.SEG_FULL
+
+
+def _large_group_batch(hq, hkv, d):
+    """Decode tokens, a 2-token step, a 16-token chunk under a window and a
+    130-row prefill, at Hq / Hkv = hq / hkv."""
+    q_lens = [1, 1, 2, 16, 130]
+    kv_lens = [700, 3000, 41, 1500, 400]
+    segs = [[(0, L, C, 0)] for L in kv_lens]
+    return W.custom(f"large_group_{hq}x{hkv}_d{d}", hq, hkv, d, q_lens, kv_lens, segs, [0, 0, 0, 600, 0], seed=7)
+
+
+@pytest.mark.parametrize("flag", list(FLAGS))
+@pytest.mark.parametrize("hq,hkv,d", [(32, 1, 128), (28, 1, 64), (64, 2, 128), (32, 4, 64)],
+                         ids=lambda v: str(v))
+def test_large_query_head_groups(hq, hkv, d, flag):
+    b = _large_group_batch(hq, hkv, d)
+    t = W.make_tensors_torch(b, DEV)
+    out, lse = run_gpu(b, t, FLAGS[flag], out_fill=float("nan"))
+    compare(b, out, lse, *oracle_of(b, t), f"{b.name}/{flag}")
+
+
+def _very_long_batch(d):
+    """A 130-row prefill at the end of 40000 keys (a full 30000-key block,
+    then causal), one decode token over 60000 causal keys and a 64-row chunk
+    over 50000 keys with a 20000-key window."""
+    q_lens = [130, 1, 64]
+    kv_lens = [40000, 60000, 50000]
+    segs = [[(0, 30000, FULL, 0), (30000, 10000, C, 0)], [(0, 60000, C, 0)], [(0, 50000, C, 0)]]
+    return W.custom(f"very_long_d{d}", 4, 2, d, q_lens, kv_lens, segs, [0, 0, 20000], seed=9)
+
+
+@pytest.mark.parametrize("flag", ["auto", "no_split"])
+@pytest.mark.parametrize("d", [64, 128])
+def test_very_long_items(d, flag):
+    b = _very_long_batch(d)
+    print(f"{b.name}/{flag}: generating", flush=True)
+    t = W.make_tensors_torch(b, DEV)
+    out, lse = run_gpu(b, t, FLAGS[flag], out_fill=float("nan"))
+    compare(b, out, lse, *oracle_of(b, t), f"{b.name}/{flag}")
