@@ -95,3 +95,36 @@ def test_zero_query_requests_leave_their_neighbours_rows_alone():
     pl.destroy()
     assert torch.isnan(out[total_q:].float()).all() and torch.isnan(lse[total_q:]).all()
     compare(b, out[:total_q], lse[:total_q], *oracle_of(b, t), "zero_query neighbours")
+
+
+@pytest.mark.parametrize("cascade", [False, True], ids=["plain", "cascade"])
+@pytest.mark.parametrize("flag", list(FLAGS))
+def test_request_rows_in_any_order_with_gaps(flag, cascade):
+    """Requests may place their packed rows anywhere in q / out / lse: here in
+    reverse request order with gaps of one to three rows between them and
+    before the first.  Every row of a request matches the oracle and every
+    row of no request keeps its NaN fill (plain plans, and cascades with
+    every group member joined)."""
+    import dataclasses
+
+    import torch
+
+    base = W.mixed(seed=4)
+    seqs = base.seqs.copy()
+    pos = 5
+    for r in reversed(range(base.num_seqs)):
+        seqs[r, 2] = pos
+        pos += int(seqs[r, 0]) + 1 + r % 3
+    b = dataclasses.replace(base, seqs=seqs, name="mixed_scattered_rows")
+    t = W.make_tensors_torch(b, DEV)
+    # as a cascade every member of the shared-prefix group joins it
+    flags = FLAGS[flag] | (attn.FLAG_CASCADE_ALL if cascade else 0)
+    out, lse = run_gpu(b, t, flags, out_fill=float("nan"), cascade=cascade)
+    rows = np.concatenate([np.arange(qs, qs + ql) for ql, _, qs in seqs.tolist()])
+    gaps = np.setdiff1d(np.arange(b.total_q), rows)
+    assert len(gaps) > 0
+    g = torch.from_numpy(gaps).to(DEV)
+    assert torch.isnan(out.index_select(0, g).float()).all() and torch.isnan(lse.index_select(0, g)).all()
+    ro, rl = oracle_of(b, t)
+    idx = torch.from_numpy(rows).to(DEV)
+    compare(b, out.index_select(0, idx), lse.index_select(0, idx), ro[rows], rl[rows], f"{b.name}/{flag}/cascade={cascade}")
