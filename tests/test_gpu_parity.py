@@ -179,14 +179,20 @@ def test_unused_slots_poisoned_with_nan():
             _compare(b, out, lse, *_oracle(b, t), f"{name} NaN-poisoned flags{flag}")
 
 
-def test_out_of_range_page_sets_error_bit_without_reading():
+@pytest.mark.parametrize("name", ["decode_bf16", "mixed", "rollout_bf16", "text_latent_bf16"])
+def test_out_of_range_page_sets_error_bit_without_reading(name):
+    """Block-table entries past the pool or negative, on the few-row path
+    (decode), the tile path at d = 64 (rollouts) and d = 128 (text+latent)
+    and both in one launch (mixed): the device error bit is set, read and
+    cleared, and every output stays finite (the bad pages read as zeros)."""
     import torch
 
-    b = W.reduced("decode_bf16")
+    b = W.reduced(name)
     t = W.make_tensors_torch(b, DEV)
     bt = b.block_table.copy()
-    bt[0, 0] = b.num_pages + 5
-    bt[1, 0] = -3
+    for r in range(b.num_seqs):
+        if b.seqs[r, 1] > 0:
+            bt[r, 0] = b.num_pages + 5 if r % 2 == 0 else -3
     pl = plan_for(b)
     out = torch.zeros_like(t["q"])
     lse = torch.zeros(t["q"].shape[:2], dtype=torch.float32, device=DEV)
