@@ -109,3 +109,26 @@ def test_full_size_append_property(name):
     keep[flat] = False
     assert torch.equal(kflat[keep].view(torch.int16), kp_before.view(-1, b.num_kv_heads, b.head_dim)[keep].view(torch.int16))
     print(f"{name}: {len(targets)} rows appended", flush=True)
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_append_on_random_batches_bitwise(seed):
+    """The seeded random batches of the attention parity test (head layouts,
+    bf16 and fp32, request shapes with and without rows, tails of any
+    length inside or across pages): the pool after the append equals the
+    oracle's bit for bit, unused slots (NaN-poisoned) included."""
+    import torch
+
+    from tests.test_gpu_random_batches import random_batch
+
+    b, _ = random_batch(seed)
+    t = W.make_tensors_torch(b, DEV, poison_unused=True)
+    kn, vn = _new_rows(b, seed=100 + seed)
+    ref_k, ref_v = kv_append(b, _host(kn), _host(vn), _host(t["k_pages"]), _host(t["v_pages"]))
+    pl = plan_for(b)
+    bt = torch.from_numpy(np.ascontiguousarray(b.block_table)).to(DEV)
+    attn.kv_append(pl, kn, vn, bt, t["k_pages"], t["v_pages"])
+    assert attn.check(pl) == 0
+    pl.destroy()
+    assert np.array_equal(_host(t["k_pages"]).view(np.uint32), ref_k.view(np.uint32)), f"seed {seed}: K pages"
+    assert np.array_equal(_host(t["v_pages"]).view(np.uint32), ref_v.view(np.uint32)), f"seed {seed}: V pages"
